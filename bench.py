@@ -1,0 +1,258 @@
+"""Benchmark of the MaxSim / InfoNCE / top-k path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
+
+Default workload: the ColTrast training step (64 queries x 32 tokens against 512 in-batch
+documents x 256 tokens, dim 128, bf16): one step = one coltrast_loss_fwd_bwd call, i.e. CSR
+partition, MaxSim scoring with the fused max/argmax, InfoNCE loss, and the dQ and dD
+gradients.  Other workloads (--workload): li_retrieval (1,024 x 32 queries against 500,000
+ragged documents, exact top-100), li_large (4,096 x 64 against 1,000,000 lognormal documents,
+top-1000), dense_retrieval (4,096 queries against 10,000,000 fp16 rows of dim 4096, top-100),
+tiny_maxsim.
+
+Prints ONE JSON line.  `value` is MaxSim query x document pairs per second for the whole step
+(queries per second for dense_retrieval) with inputs resident in HBM.  `roofline` describes the
+dominant kernel: algorithmic FLOPs per launch over its average duration, measured with HIP
+events recorded by the library around each of its launches during the timed region.
+`cpu_baseline` is the fp64 oracle timed on this host on a bounded sample of the same workload.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 / fp16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="coltrast_step",
+                    choices=["coltrast_step", "li_retrieval", "li_large", "dense_retrieval",
+                             "tiny_maxsim"])
+    ap.add_argument("--logit-scale", type=float, default=1.5625,
+                    help="inverse temperature of the InfoNCE logits (coltrast_step)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the extra HIP-graph replay timing of the same step")
+    return ap.parse_args()
+
+
+def source_sha(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2505_04846_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic(kernel, workload, sha):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if still current."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        recs = json.load(f)
+    for r in recs:
+        if r.get("kernel") == kernel and r.get("workload") == workload and r.get("source_sha") == sha:
+            return r.get("hbm_bytes_per_launch")
+    return None
+
+
+def blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        n = [i.get("num_threads", 0) for i in threadpool_info() if i.get("user_api") == "blas"]
+        if n:
+            return max(n)
+    except Exception:
+        pass
+    return len(os.sched_getaffinity(0))
+
+
+def build_workload(name, dev, scale):
+    import torch
+    import paper_2505_04846_amd as hpr
+    import synth
+
+    if name in ("coltrast_step",):
+        w = synth.coltrast_step(seed=0, device="cpu")
+        Q, D, off, pos = (w[k].to(dev) for k in ("Q", "D", "off", "pos"))
+        nq, lq, dim = Q.shape
+        n_docs = off.numel() - 1
+        ws = hpr.coltrast_workspace(Q, D, off)
+        out = {"loss": torch.empty(1, dtype=torch.float32, device=dev),
+               "dq": torch.empty(Q.shape, dtype=torch.float32, device=dev),
+               "dd": torch.empty(D.shape, dtype=torch.float32, device=dev)}
+
+        def step():
+            hpr.coltrast_loss_fwd_bwd(Q, D, off, pos, scale, ws=ws, out=out)
+
+        lens = (w["off"][1:] - w["off"][:-1]).to(torch.float64)
+        flops = 2.0 * dim * lq * nq * float(lens.sum())
+
+        def cpu_sample():
+            import oracle
+            bf = lambda t: oracle.decode_bf16(t.view(torch.int16).numpy())
+            t0 = time.perf_counter()
+            oracle.coltrast_li_loss(bf(w["Q"]), bf(w["D"]), w["off"].numpy(), w["pos"].numpy(),
+                                    scale)
+            dt = time.perf_counter() - t0
+            return nq * n_docs / dt, "the full workload once: loss, dQ and dD (64 x 512 pairs)"
+
+        cfg = {"workload": "coltrast_step", "nq": nq, "lq": lq, "n_docs": n_docs, "ld": 256,
+               "dim": dim, "hard_negatives_per_query": 7, "logit_scale": scale}
+        return dict(step=step, pairs=nq * n_docs, kernel="maxsim_argmax", flops=flops,
+                    cpu_sample=cpu_sample, config=cfg, dtype="bf16", unit="pairs/s",
+                    sha=source_sha("maxsim.hip", "common.h"))
+
+    if name in ("li_retrieval", "li_large", "tiny_maxsim"):
+        if name == "li_retrieval":
+            w = synth.li_retrieval(seed=0, device=dev)
+        elif name == "li_large":
+            w = synth.li_large(seed=0, device=dev)
+        else:
+            w = synth.tiny_maxsim(seed=0, device=dev)
+        Q, D, off, k = w["Q"], w["D"], w["off"], w["k"]
+        nq, lq, dim = Q.shape
+        n_docs = off.numel() - 1
+        n_tok = D.shape[0]
+        ws = torch.empty(hpr.lib().maxsim_topk_workspace_size(nq, lq, n_docs, n_tok, dim, k),
+                         dtype=torch.uint8, device=dev)
+
+        def step():
+            hpr.maxsim_topk(Q, D, off, k, ws=ws)
+
+        flops = 2.0 * dim * lq * nq * float(n_tok)
+
+        def cpu_sample():
+            import oracle
+            bf = lambda t: oracle.decode_bf16(t.cpu().view(torch.int16).numpy())
+            qs = 1 if n_docs > 10000 else nq
+            Dh, offh, Qh = bf(D), off.cpu().numpy(), bf(Q[:qs])
+            t0 = time.perf_counter()
+            S = oracle.maxsim_scores(Qh, Dh, offh)
+            oracle.rank_topk(S, k)
+            dt = time.perf_counter() - t0
+            return qs * n_docs / dt, f"{qs} quer{'y' if qs == 1 else 'ies'} against every document, scores + top-{k}"
+
+        cfg = {"workload": name, "nq": nq, "lq": lq, "n_docs": n_docs, "n_tok": n_tok,
+               "dim": dim, "k": k}
+        return dict(step=step, pairs=nq * n_docs, kernel="maxsim", flops=flops,
+                    cpu_sample=cpu_sample, config=cfg, dtype="bf16", unit="pairs/s",
+                    sha=source_sha("maxsim.hip", "common.h"))
+
+    raise SystemExit(f"workload {name} is not available in this build")
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the sharding design is described in DESIGN.md); run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2505_04846_amd as hpr
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    W = build_workload(args.workload, dev, args.logit_scale)
+    print(f"[bench] workload {args.workload} ready", file=sys.stderr, flush=True)
+
+    for _ in range(args.warmup):
+        W["step"]()
+    torch.cuda.synchronize()
+
+    hpr.kernel_timing(True)
+    for name in ("partition", "maxsim", "maxsim_argmax", "topk", "infonce", "grad_q", "grad_d"):
+        hpr.kernel_timing_read(name)  # drop warm-up records (timing was off; no-op)
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        W["step"]()
+    stop.record()
+    torch.cuda.synchronize()
+    hpr.kernel_timing(False)
+    ms = start.elapsed_time(stop) / args.steps
+
+    graph_ms = None
+    if not args.no_graph:
+        # the same step captured once in a HIP graph and replayed (launch overhead removed)
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            W["step"]()
+        torch.cuda.current_stream().wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            W["step"]()
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(args.steps):
+            g.replay()
+        stop.record()
+        torch.cuda.synchronize()
+        graph_ms = start.elapsed_time(stop) / args.steps
+
+    kernels = {}
+    for name in ("partition", "maxsim", "maxsim_argmax", "topk", "infonce", "grad_q", "grad_d"):
+        tot, n = hpr.kernel_timing_read(name)
+        if n:
+            kernels[name] = {"avg_us": round(1e3 * tot / n, 3), "launches": n}
+    kname = W["kernel"]
+    k_avg_s = kernels[kname]["avg_us"] * 1e-6
+    achieved = W["flops"] / k_avg_s / 1e12
+    roofline = {
+        "bound": "mfma", "kernel": kname, "achieved": round(achieved, 2),
+        "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+        "traffic": committed_traffic(kname, args.workload, W["sha"]),
+        "flops_per_launch": W["flops"], "avg_launch_us": kernels[kname]["avg_us"],
+    }
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        v, sample = W["cpu_sample"]()
+        cpu = {"value": v, "unit": W["unit"], "cores": blas_threads(), "kind": "oracle",
+               "sample": sample}
+
+    line = {
+        "metric": "MaxSim query x doc pairs/sec + % bf16 MFMA peak",
+        "value": W["pairs"] / (ms * 1e-3),
+        "unit": W["unit"],
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": W["dtype"],
+        "data": "synthetic",
+        "config": W["config"],
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+        "graph_replay": None if graph_ms is None else {
+            "ms_per_step": graph_ms, "value": W["pairs"] / (graph_ms * 1e-3)},
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,196 @@
+/*
+ * hiperrag.h -- C ABI of the MI355X (gfx950) late-interaction scoring, InfoNCE and exact top-k
+ * library.  It implements the data-parallel core of the ColTrast retrieval path of HiPerRAG
+ * (arXiv 2505.04846).
+ *
+ * The operations (see each entry point for its defining passage in the paper):
+ *   maxsim_score           late-interaction (MaxSim) scores of every query against every
+ *                          document of a CSR token store.
+ *   maxsim_topk            exact top-k documents per query under MaxSim.
+ *   coltrast_loss_fwd_bwd  in-batch InfoNCE loss over MaxSim scores (the L_LI half of the
+ *                          ColTrast loss) with its gradients.
+ *   dense_ip_topk          exact top-k rows of a pooled-embedding store by inner product
+ *                          (= cosine for L2-normalised rows).
+ *
+ * Conventions shared by every entry point
+ *   Pointers.  Every array argument is a DEVICE pointer on the current HIP device, owned by
+ *     the caller, unless it is marked [host].  bf16 and fp16 values are passed as raw 16-bit
+ *     patterns (uint16_t).  `stream` is a hipStream_t passed as void* (NULL = the default
+ *     stream).
+ *   Layouts.  Row-major and dense.  Queries Q are [nq, lq, dim]; the document store is CSR:
+ *     tokens d_tok [n_tok, dim] and offsets d_off [n_docs + 1] (int64), the tokens of
+ *     document d being rows d_off[d] .. d_off[d+1]-1.
+ *   Asynchrony.  Every compute call only validates its arguments on the host (O(1), no device
+ *     reads, no synchronisation) and enqueues kernels on `stream`; results are valid once the
+ *     stream has reached that point.  Device faults surface at the caller's next
+ *     synchronisation, as in HIP.
+ *   Memory.  The library never allocates device memory.  Scratch space comes from the caller as
+ *     a workspace `ws` of `ws_bytes` bytes (256-byte aligned), sized by the matching
+ *     *_workspace_size() query.  A workspace may be reused by later calls on the same stream;
+ *     concurrent calls need distinct workspaces.
+ *   Preconditions not checked by the compute calls (checking them would need a device read and
+ *     a synchronisation): the CSR offsets are valid (d_off[0] = 0, strictly increasing,
+ *     d_off[n_docs] = n_tok, so every document has at least one token; hpr_csr_validate checks
+ *     this) and every input value is finite.  Violating them gives unspecified results but no
+ *     out-of-bounds access.
+ *   Errors.  A status code is returned and no exception crosses the ABI; hpr_last_error()
+ *     describes the last non-OK status of the calling thread.
+ *   Alignment.  Every device pointer must be 16-byte aligned.
+ *   Threads.  Entry points are reentrant.
+ */
+#ifndef HIPERRAG_H
+#define HIPERRAG_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t hpr_status;
+
+#define HPR_OK 0
+#define HPR_ERR_INVALID_ARG 1         /* NULL pointer, non-positive size, k out of range ...   */
+#define HPR_ERR_BAD_CSR 2             /* hpr_csr_validate: offsets not a valid CSR             */
+#define HPR_ERR_EMPTY_DOC 3           /* hpr_csr_validate: a document with no token            */
+#define HPR_ERR_UNSUPPORTED_SHAPE 4   /* valid, but outside the limits this build supports     */
+#define HPR_ERR_WORKSPACE_TOO_SMALL 5 /* ws_bytes below the *_workspace_size() value            */
+#define HPR_ERR_HIP 7                 /* a HIP runtime call or kernel launch failed             */
+
+#define HPR_ABI_VERSION 1
+
+/* Shape limits of this build (HPR_ERR_UNSUPPORTED_SHAPE beyond them).
+ *   MaxSim calls: dim % 8 == 0, 8 <= dim <= 256; lq <= 128 when dim <= 128, lq <= 64 when
+ *     dim <= 256; coltrast_loss_fwd_bwd: lq <= 64.
+ *   Top-k: 1 <= k <= min(n, 1024) (k outside that range is HPR_ERR_INVALID_ARG).
+ *   coltrast_loss_fwd_bwd: nq * lq <= 16384 and every document has at most 65536 tokens (the
+ *     latter is checked on the device: a longer document makes *loss NaN).
+ *   dense_ip_topk: dim % 8 == 0, 8 <= dim <= 8192.
+ */
+
+/* ---------------------------------------------------------------------------------------------
+ * maxsim_score -- late-interaction (MaxSim) scores.
+ *
+ * Defined by the late-interaction mechanism (Sec. 2.2, and Sec. 3.2.1 with Fig. 3B): every query
+ * token is compared with every token of the document, keeps its largest inner product, and the
+ * per-token maxima are summed over the query tokens:
+ *     scores[q * n_docs + d] = sum_{i < lq} max_{d_off[d] <= j < d_off[d+1]} <Q[q,i,:], D[j,:]>
+ * Arithmetic: bf16 x bf16 products accumulated in fp32 (MFMA); max and sum in fp32; the sum
+ * over i is taken in a fixed order, so results are bit-reproducible and do not depend on the
+ * order of a document's tokens.
+ *
+ *   q      bf16 [nq, lq, dim]        query token embeddings
+ *   d_tok  bf16 [n_tok, dim]         document token embeddings (CSR rows)
+ *   d_off  int64 [n_docs + 1]        CSR offsets
+ *   scores fp32 [nq, n_docs]         output, fully overwritten
+ *   ws     workspace of maxsim_score_workspace_size(...) bytes
+ * ------------------------------------------------------------------------------------------- */
+hpr_status maxsim_score(const uint16_t* q, int32_t nq, int32_t lq,
+                        const uint16_t* d_tok, const int64_t* d_off, int64_t n_docs,
+                        int64_t n_tok, int32_t dim, float* scores,
+                        void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------------------------
+ * maxsim_topk -- exact top-k documents of each query under MaxSim.
+ *
+ * Retrieval returns the IDs of a query's nearest neighbours in the chunk store (Sec. 2.3);
+ * scored here with the late-interaction score of maxsim_score, over every document (exact, no
+ * candidate pre-filter).  Results per query are sorted by score descending, equal scores by
+ * lower document index first (-0.0 and +0.0 are equal).
+ *
+ *   out_scores fp32 [nq, k]; out_idx int64 [nq, k] (document indices in [0, n_docs)).
+ *   ws     workspace of maxsim_topk_workspace_size(...) bytes (it holds the [nq, n_docs] fp32
+ *          score matrix).
+ * ------------------------------------------------------------------------------------------- */
+hpr_status maxsim_topk(const uint16_t* q, int32_t nq, int32_t lq,
+                       const uint16_t* d_tok, const int64_t* d_off, int64_t n_docs,
+                       int64_t n_tok, int32_t dim, int32_t k,
+                       float* out_scores, int64_t* out_idx,
+                       void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------------------------
+ * coltrast_loss_fwd_bwd -- in-batch InfoNCE over MaxSim scores, forward and backward.
+ *
+ * The ColTrast loss is L = (L_LI + L_C) / 2 with L_LI the MaxSim loss of ColBERT applied to the
+ * local batch only (Sec. 3.2.1, "Embedding performance: loss function").  This call computes
+ * L_LI as a softmax cross-entropy of every query against all n_docs documents of the batch:
+ *     l[q,d]  = logit_scale * S[q,d]                       (S as in maxsim_score)
+ *     loss    = (1/nq) sum_q ( log sum_d exp(l[q,d]) - l[q, pos_idx[q]] )
+ *     G[q,d]  = (logit_scale/nq) * (softmax_d(l[q,:])[d] - [d == pos_idx[q]])
+ *     dq[q,i,:] = sum_d G[q,d] * D[a(q,i,d), :]
+ *     dd[j,:]   = sum over (q,i,d) with a(q,i,d) = j of G[q,d] * Q[q,i,:]
+ * where a(q,i,d) is the lowest-index token of document d attaining query token (q,i)'s maximum.
+ * Gradients are with respect to the bf16 inputs taken as real numbers.
+ *
+ *   pos_idx     int32 [nq], positives; an out-of-range entry makes *loss NaN (device check).
+ *   logit_scale the inverse temperature s.
+ *   loss        fp32 [1] output (stays on the device).
+ *   dq          fp32 [nq, lq, dim] output, or NULL to skip it.
+ *   dd          fp32 [n_tok, dim] output (every row written; rows no query token selects are 0),
+ *               or NULL to skip it.
+ *   scores      fp32 [nq, n_docs] optional copy of S, or NULL.
+ *   The dd reduction is deterministic (fixed summation order): repeated calls give identical
+ *   bits.
+ * ------------------------------------------------------------------------------------------- */
+hpr_status coltrast_loss_fwd_bwd(const uint16_t* q, int32_t nq, int32_t lq,
+                                 const uint16_t* d_tok, const int64_t* d_off, int64_t n_docs,
+                                 int64_t n_tok, int32_t dim,
+                                 const int32_t* pos_idx, float logit_scale,
+                                 float* loss, float* dq, float* dd, float* scores,
+                                 void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------------------------
+ * dense_ip_topk -- exact top-k rows of a pooled-embedding store by inner product.
+ *
+ * At query time the paper ranks chunks by the cosine between the pooled question embedding and
+ * each pooled chunk embedding and returns the nearest neighbours' IDs (Sec. 3.2.1 "Similarity
+ * metric"; Sec. 4.2; Sec. 2.3).  For L2-normalised rows the cosine is the inner product:
+ *     s[q,n] = <Q[q,:], X[n,:]>  (fp16 x fp16 products, fp32 accumulation)
+ * Results are sorted by score descending, equal scores by lower row index first.
+ *
+ *   q   fp16 [nq, dim]; x fp16 [n, dim]; out_scores fp32 [nq, k]; out_idx int64 [nq, k].
+ * ------------------------------------------------------------------------------------------- */
+hpr_status dense_ip_topk(const uint16_t* q, int32_t nq, const uint16_t* x, int64_t n,
+                         int32_t dim, int32_t k, float* out_scores, int64_t* out_idx,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace sizes in bytes for the calls above (0 is a valid size only when stated). */
+size_t maxsim_score_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int64_t n_tok,
+                                   int32_t dim);
+size_t maxsim_topk_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int64_t n_tok,
+                                  int32_t dim, int32_t k);
+size_t coltrast_loss_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int64_t n_tok,
+                                    int32_t dim);
+size_t dense_ip_topk_workspace_size(int32_t nq, int64_t n, int32_t dim, int32_t k);
+
+/* ---------------------------------------------------------------------------------------------
+ * hpr_csr_validate -- checks a CSR offsets array on the device and SYNCHRONISES `stream`.
+ *   Returns HPR_OK, HPR_ERR_BAD_CSR (d_off[0] != 0, d_off[n_docs] != n_tok, or a decrease) or
+ *   HPR_ERR_EMPTY_DOC (two equal neighbours).  *h_first_bad_doc [host] receives the lowest
+ *   offending document index, or -1.  ws needs 16 bytes.
+ * ------------------------------------------------------------------------------------------- */
+hpr_status hpr_csr_validate(const int64_t* d_off, int64_t n_docs, int64_t n_tok, void* ws,
+                            void* stream, int64_t* h_first_bad_doc);
+
+/* hpr_scale_f32 -- x[i] *= *scale for i < n (scale is a device scalar); used to apply an
+ * upstream gradient to the gradients of coltrast_loss_fwd_bwd without a host round trip. */
+hpr_status hpr_scale_f32(float* x, int64_t n, const float* scale, void* stream);
+
+/* Per-kernel timing for benchmarks.  While enabled, every kernel the library launches is
+ * bracketed by two HIP events recorded on its launch stream.  hpr_kernel_timing_read
+ * synchronises on the events recorded for kernel `name` ("partition", "maxsim",
+ * "maxsim_argmax", "topk", "infonce", "grad_q", "grad_d", "dense_scan", "dense_merge"), returns
+ * the sum of their durations in milliseconds and the launch count, and forgets them. */
+hpr_status hpr_kernel_timing(int32_t enable);
+hpr_status hpr_kernel_timing_read(const char* name, double* total_ms, int64_t* launches);
+
+const char* hpr_status_string(hpr_status s);
+const char* hpr_last_error(void); /* thread-local description of the last non-OK status */
+int32_t hpr_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HIPERRAG_H */

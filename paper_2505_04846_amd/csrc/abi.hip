@@ -1,0 +1,360 @@
+// C ABI of the library: host-side argument validation, workspace carving and kernel dispatch.
+// Validation never touches the device, so every error path below runs without a GPU.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "hiperrag.h"
+#include "kernels.h"
+
+using namespace hpr;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+hpr_status fail(hpr_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+hpr_status hip_fail(hipError_t e, const char* where) {
+  return fail(HPR_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cu_count[kMaxDevices];
+
+// Compute-unit count of the current device (cached per device).
+hpr_status current_cu_count(int* n_cu) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev >= 0 && dev < kMaxDevices) {
+    const int c = g_cu_count[dev].load(std::memory_order_relaxed);
+    if (c > 0) {
+      *n_cu = c;
+      return HPR_OK;
+    }
+  }
+  int c = 0;
+  e = hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+  if (dev >= 0 && dev < kMaxDevices) g_cu_count[dev].store(c, std::memory_order_relaxed);
+  *n_cu = c;
+  return HPR_OK;
+}
+
+// Optional per-kernel timing: when enabled, every launch made through `timed` is bracketed by
+// two HIP events recorded on the launch stream; hpr_kernel_timing_read sums their durations.
+std::atomic<int> g_timing_on{0};
+std::mutex g_timing_mu;
+std::map<std::string, std::vector<std::pair<hipEvent_t, hipEvent_t>>> g_timing;
+
+template <class F>
+hipError_t timed(const char* name, hipStream_t s, F&& launch) {
+  if (!g_timing_on.load(std::memory_order_relaxed)) return launch();
+  hipEvent_t a = nullptr, b = nullptr;
+  if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return launch();
+  (void)hipEventRecord(a, s);
+  const hipError_t e = launch();
+  (void)hipEventRecord(b, s);
+  std::lock_guard<std::mutex> g(g_timing_mu);
+  g_timing[name].emplace_back(a, b);
+  return e;
+}
+
+// Shared checks of the MaxSim calls (query tensor + CSR store).
+hpr_status check_maxsim_args(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d_tok,
+                             const int64_t* d_off, int64_t n_docs, int64_t n_tok, int32_t dim) {
+  if (!q || !d_tok || !d_off) return fail(HPR_ERR_INVALID_ARG, "q, d_tok and d_off must be non-NULL");
+  if (nq < 1 || lq < 1) return fail(HPR_ERR_INVALID_ARG, "nq (%d) and lq (%d) must be >= 1", nq, lq);
+  if (n_docs < 1) return fail(HPR_ERR_INVALID_ARG, "n_docs (%lld) must be >= 1", (long long)n_docs);
+  if (n_tok < n_docs)
+    return fail(HPR_ERR_INVALID_ARG, "n_tok (%lld) < n_docs (%lld): every document needs a token",
+                (long long)n_tok, (long long)n_docs);
+  if (dim < 1) return fail(HPR_ERR_INVALID_ARG, "dim (%d) must be >= 1", dim);
+  if (dim % 8 != 0 || dim < 8 || dim > 256)
+    return fail(HPR_ERR_UNSUPPORTED_SHAPE, "MaxSim needs dim %% 8 == 0 and 8 <= dim <= 256 (dim=%d)", dim);
+  if ((int64_t)nq * n_docs > (int64_t(1) << 40))
+    return fail(HPR_ERR_UNSUPPORTED_SHAPE, "nq * n_docs too large");
+  if (!aligned16(q) || !aligned16(d_tok) || !aligned16(d_off))
+    return fail(HPR_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+  return HPR_OK;
+}
+
+// Query-length limit of the MaxSim kernels (query slots a wave holds).
+hpr_status check_lq(int32_t lq, int32_t dim, bool argmax) {
+  const int lqp = (lq + 15) / 16 * 16;
+  const int max_slots = (dim <= 128 && !argmax) ? 128 : 64;
+  if (lqp > max_slots)
+    return fail(HPR_ERR_UNSUPPORTED_SHAPE, "lq=%d exceeds the limit %d for dim=%d%s", lq,
+                max_slots, dim, argmax ? " in the loss" : "");
+  return HPR_OK;
+}
+
+size_t part_bytes(int64_t n_docs) {
+  const int64_t r = n_docs < kMaxRanges ? n_docs : kMaxRanges;
+  return align_up((size_t)(r + 1) * sizeof(int64_t));
+}
+
+// Carves consecutive 256-byte aligned regions out of a workspace.
+struct Carver {
+  char* base;
+  size_t used = 0;
+  explicit Carver(void* ws) : base(static_cast<char*>(ws)) {}
+  template <class T>
+  T* take(size_t bytes) {
+    T* p = reinterpret_cast<T*>(base + used);
+    used += align_up(bytes);
+    return p;
+  }
+};
+
+hpr_status run_maxsim(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d_tok,
+                      const int64_t* d_off, int64_t n_docs, int64_t n_tok, int32_t dim,
+                      float* scores, uint16_t* amax, int32_t* flag, int64_t* part,
+                      hipStream_t stream) {
+  int n_cu = 0;
+  hpr_status st = current_cu_count(&n_cu);
+  if (st != HPR_OK) return st;
+  MaxsimPlan plan;
+  if (!maxsim_plan(nq, lq, n_docs, n_tok, dim, amax != nullptr, n_cu, &plan))
+    return fail(HPR_ERR_UNSUPPORTED_SHAPE, "no MaxSim plan for this shape");
+  hipError_t e = timed("partition", stream, [&] {
+    return launch_partition(d_off, n_docs, n_tok, plan.n_ranges, part, flag, stream);
+  });
+  if (e != hipSuccess) return hip_fail(e, "partition launch");
+  e = timed(amax ? "maxsim_argmax" : "maxsim", stream, [&] {
+    return launch_maxsim(plan, q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, part, scores, amax,
+                         flag, stream);
+  });
+  if (e != hipSuccess) return hip_fail(e, "maxsim launch");
+  return HPR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t maxsim_score_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int64_t n_tok,
+                                   int32_t dim) {
+  (void)nq, (void)lq, (void)n_tok, (void)dim;
+  return n_docs < 1 ? 0 : part_bytes(n_docs);
+}
+
+size_t maxsim_topk_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int64_t n_tok,
+                                  int32_t dim, int32_t k) {
+  (void)lq, (void)n_tok, (void)dim, (void)k;
+  if (nq < 1 || n_docs < 1) return 0;
+  return align_up((size_t)nq * (size_t)n_docs * sizeof(float)) + part_bytes(n_docs);
+}
+
+size_t coltrast_loss_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int64_t n_tok,
+                                    int32_t dim) {
+  (void)n_tok, (void)dim;
+  if (nq < 1 || lq < 1 || n_docs < 1) return 0;
+  const size_t sd = align_up((size_t)nq * (size_t)n_docs * sizeof(float));
+  const size_t am = align_up((size_t)n_docs * (size_t)nq * (size_t)lq * sizeof(uint16_t));
+  return 2 * sd + am + part_bytes(n_docs) + align_up(2 * sizeof(int32_t)) +
+         align_up((size_t)nq * sizeof(float));
+}
+
+hpr_status maxsim_score(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d_tok,
+                        const int64_t* d_off, int64_t n_docs, int64_t n_tok, int32_t dim,
+                        float* scores, void* ws, size_t ws_bytes, void* stream) {
+  hpr_status st = check_maxsim_args(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim);
+  if (st == HPR_OK) st = check_lq(lq, dim, false);
+  if (st != HPR_OK) return st;
+  if (!scores || !ws) return fail(HPR_ERR_INVALID_ARG, "scores and ws must be non-NULL");
+  const size_t need = maxsim_score_workspace_size(nq, lq, n_docs, n_tok, dim);
+  if (ws_bytes < need)
+    return fail(HPR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu < %zu bytes", ws_bytes, need);
+  Carver c(ws);
+  int64_t* part = c.take<int64_t>(part_bytes(n_docs));
+  return run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, scores, nullptr, nullptr, part,
+                    static_cast<hipStream_t>(stream));
+}
+
+hpr_status maxsim_topk(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d_tok,
+                       const int64_t* d_off, int64_t n_docs, int64_t n_tok, int32_t dim,
+                       int32_t k, float* out_scores, int64_t* out_idx, void* ws,
+                       size_t ws_bytes, void* stream) {
+  hpr_status st = check_maxsim_args(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim);
+  if (st == HPR_OK) st = check_lq(lq, dim, false);
+  if (st != HPR_OK) return st;
+  if (!out_scores || !out_idx || !ws)
+    return fail(HPR_ERR_INVALID_ARG, "out_scores, out_idx and ws must be non-NULL");
+  if (k < 1 || k > 1024 || (int64_t)k > n_docs)
+    return fail(HPR_ERR_INVALID_ARG, "k=%d must satisfy 1 <= k <= min(n_docs, 1024)", k);
+  const size_t need = maxsim_topk_workspace_size(nq, lq, n_docs, n_tok, dim, k);
+  if (ws_bytes < need)
+    return fail(HPR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu < %zu bytes", ws_bytes, need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Carver c(ws);
+  float* scores = c.take<float>((size_t)nq * n_docs * sizeof(float));
+  int64_t* part = c.take<int64_t>(part_bytes(n_docs));
+  st = run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, scores, nullptr, nullptr, part, s);
+  if (st != HPR_OK) return st;
+  hipError_t e = timed("topk", s, [&] {
+    return launch_topk_rows(scores, nq, n_docs, n_docs, k, out_scores, out_idx, s);
+  });
+  if (e != hipSuccess) return hip_fail(e, "top-k launch");
+  return HPR_OK;
+}
+
+hpr_status coltrast_loss_fwd_bwd(const uint16_t* q, int32_t nq, int32_t lq,
+                                 const uint16_t* d_tok, const int64_t* d_off, int64_t n_docs,
+                                 int64_t n_tok, int32_t dim, const int32_t* pos_idx,
+                                 float logit_scale, float* loss, float* dq, float* dd,
+                                 float* scores, void* ws, size_t ws_bytes, void* stream) {
+  hpr_status st = check_maxsim_args(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim);
+  if (st == HPR_OK) st = check_lq(lq, dim, true);
+  if (st != HPR_OK) return st;
+  if (!pos_idx || !loss || !ws) return fail(HPR_ERR_INVALID_ARG, "pos_idx, loss and ws must be non-NULL");
+  if (!(logit_scale == logit_scale) || logit_scale > 3.0e38f || logit_scale < -3.0e38f)
+    return fail(HPR_ERR_INVALID_ARG, "logit_scale must be finite");
+  if ((int64_t)nq * lq > 16384)
+    return fail(HPR_ERR_UNSUPPORTED_SHAPE, "nq * lq = %lld exceeds 16384", (long long)nq * lq);
+  if ((dq && !aligned16(dq)) || (dd && !aligned16(dd)))
+    return fail(HPR_ERR_INVALID_ARG, "gradient outputs must be 16-byte aligned");
+  const size_t need = coltrast_loss_workspace_size(nq, lq, n_docs, n_tok, dim);
+  if (ws_bytes < need)
+    return fail(HPR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu < %zu bytes", ws_bytes, need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Carver c(ws);
+  float* S = c.take<float>((size_t)nq * n_docs * sizeof(float));
+  float* G = c.take<float>((size_t)nq * n_docs * sizeof(float));
+  uint16_t* amax = c.take<uint16_t>((size_t)n_docs * nq * lq * sizeof(uint16_t));
+  int64_t* part = c.take<int64_t>(part_bytes(n_docs));
+  int32_t* ctrl = c.take<int32_t>(2 * sizeof(int32_t));
+  float* terms = c.take<float>((size_t)nq * sizeof(float));
+  st = run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, S, amax, ctrl, part, s);
+  if (st != HPR_OK) return st;
+  hipError_t e = timed("infonce", s, [&] {
+    return launch_infonce(S, nq, n_docs, pos_idx, logit_scale, G, terms, loss, scores, ctrl, s);
+  });
+  if (e != hipSuccess) return hip_fail(e, "infonce launch");
+  if (dq) {
+    e = timed("grad_q", s, [&] {
+      return launch_grad_q(d_tok, d_off, n_docs, n_tok, dim, nq, lq, amax, G, dq, s);
+    });
+    if (e != hipSuccess) return hip_fail(e, "dQ launch");
+  }
+  if (dd) {
+    e = timed("grad_d", s, [&] {
+      return launch_grad_d(q, d_off, n_docs, n_tok, dim, nq, lq, amax, G, dd, s);
+    });
+    if (e != hipSuccess) return hip_fail(e, "dD launch");
+  }
+  return HPR_OK;
+}
+
+size_t dense_ip_topk_workspace_size(int32_t nq, int64_t n, int32_t dim, int32_t k) {
+  (void)nq, (void)n, (void)dim, (void)k;
+  return 0;
+}
+
+hpr_status dense_ip_topk(const uint16_t* q, int32_t nq, const uint16_t* x, int64_t n,
+                         int32_t dim, int32_t k, float* out_scores, int64_t* out_idx, void* ws,
+                         size_t ws_bytes, void* stream) {
+  (void)q, (void)nq, (void)x, (void)n, (void)dim, (void)k, (void)out_scores, (void)out_idx;
+  (void)ws, (void)ws_bytes, (void)stream;
+  return fail(HPR_ERR_UNSUPPORTED_SHAPE, "dense_ip_topk is not built yet");
+}
+
+hpr_status hpr_csr_validate(const int64_t* d_off, int64_t n_docs, int64_t n_tok, void* ws,
+                            void* stream, int64_t* h_first_bad_doc) {
+  if (!d_off || !ws || !h_first_bad_doc)
+    return fail(HPR_ERR_INVALID_ARG, "d_off, ws and h_first_bad_doc must be non-NULL");
+  if (n_docs < 1 || n_tok < 0)
+    return fail(HPR_ERR_INVALID_ARG, "n_docs must be >= 1 and n_tok >= 0");
+  *h_first_bad_doc = -1;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned long long* bad = static_cast<unsigned long long*>(ws);
+  hipError_t e = launch_csr_validate(d_off, n_docs, n_tok, bad, s);
+  if (e != hipSuccess) return hip_fail(e, "csr validate launch");
+  unsigned long long h = 0;
+  e = hipMemcpyAsync(&h, bad, sizeof(h), hipMemcpyDeviceToHost, s);
+  if (e != hipSuccess) return hip_fail(e, "csr validate copy");
+  e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "csr validate sync");
+  if (h == ~0ull) return HPR_OK;
+  *h_first_bad_doc = (int64_t)(h >> 1);
+  if (h & 1ull)
+    return fail(HPR_ERR_EMPTY_DOC, "document %lld has no token", (long long)(h >> 1));
+  return fail(HPR_ERR_BAD_CSR, "offsets invalid at document %lld", (long long)(h >> 1));
+}
+
+hpr_status hpr_scale_f32(float* x, int64_t n, const float* scale, void* stream) {
+  if (!x || !scale) return fail(HPR_ERR_INVALID_ARG, "x and scale must be non-NULL");
+  if (n < 0) return fail(HPR_ERR_INVALID_ARG, "n must be >= 0");
+  if (n == 0) return HPR_OK;
+  hipError_t e = launch_scale(x, n, scale, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "scale launch");
+  return HPR_OK;
+}
+
+hpr_status hpr_kernel_timing(int32_t enable) {
+  g_timing_on.store(enable ? 1 : 0, std::memory_order_relaxed);
+  return HPR_OK;
+}
+
+hpr_status hpr_kernel_timing_read(const char* name, double* total_ms, int64_t* launches) {
+  if (!name || !total_ms || !launches)
+    return fail(HPR_ERR_INVALID_ARG, "name, total_ms and launches must be non-NULL");
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> ev;
+  {
+    std::lock_guard<std::mutex> g(g_timing_mu);
+    auto it = g_timing.find(name);
+    if (it != g_timing.end()) ev.swap(it->second);
+  }
+  double tot = 0.0;
+  hpr_status st = HPR_OK;
+  for (auto& p : ev) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(p.second);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, p.first, p.second);
+    if (e != hipSuccess && st == HPR_OK) st = hip_fail(e, "kernel timing");
+    tot += ms;
+    (void)hipEventDestroy(p.first);
+    (void)hipEventDestroy(p.second);
+  }
+  *total_ms = tot;
+  *launches = (int64_t)ev.size();
+  return st;
+}
+
+const char* hpr_status_string(hpr_status s) {
+  switch (s) {
+    case HPR_OK: return "HPR_OK";
+    case HPR_ERR_INVALID_ARG: return "HPR_ERR_INVALID_ARG";
+    case HPR_ERR_BAD_CSR: return "HPR_ERR_BAD_CSR";
+    case HPR_ERR_EMPTY_DOC: return "HPR_ERR_EMPTY_DOC";
+    case HPR_ERR_UNSUPPORTED_SHAPE: return "HPR_ERR_UNSUPPORTED_SHAPE";
+    case HPR_ERR_WORKSPACE_TOO_SMALL: return "HPR_ERR_WORKSPACE_TOO_SMALL";
+    case HPR_ERR_HIP: return "HPR_ERR_HIP";
+    default: return "HPR_ERR_UNKNOWN";
+  }
+}
+
+const char* hpr_last_error(void) { return g_last_error.c_str(); }
+
+int32_t hpr_abi_version(void) { return HPR_ABI_VERSION; }
+
+}  // extern "C"

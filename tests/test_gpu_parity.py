@@ -1,0 +1,331 @@
+"""GPU parity: every entry point of the HIP library against the fp64 oracle on seeded inputs.
+
+Tolerances (scores and loss): |gpu - oracle| <= 2e-3 * max(|oracle|, 1e-3), the bound the task
+sets for bf16 inputs with fp32 accumulation; a 20x tighter check (1e-4) is also asserted on
+MaxSim scores because bf16 x bf16 products are exact in fp32 and only the fp32 summation differs
+from the oracle.  Gradients: per-tensor relative L2 error <= 2e-3.  Top-k lists: the rules of
+tests/topk_check.py.  Integer outputs (argmax-dependent structure, indices of clear winners)
+are compared exactly.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2505_04846_amd as hpr
+import synth
+from topk_check import check_topk
+
+pytestmark = pytest.mark.gpu
+
+REL = 2e-3
+DEV = "cuda:0"
+
+
+def _bf(t):
+    return oracle.decode_bf16(t.detach().cpu().contiguous().view(torch.int16).numpy())
+
+
+def _assert_close(g, o, rel=REL, what=""):
+    g = np.asarray(g, dtype=np.float64)
+    o = np.asarray(o, dtype=np.float64)
+    err = np.abs(g - o)
+    lim = rel * np.maximum(np.abs(o), 1e-3)
+    bad = err > lim
+    assert not bad.any(), (f"{what}: {bad.sum()} of {bad.size} outside rel {rel}; worst "
+                           f"{(err / lim).max():.3g}x the bound")
+
+
+def _rel_l2(g, o):
+    g = np.asarray(g, dtype=np.float64)
+    o = np.asarray(o, dtype=np.float64)
+    return float(np.linalg.norm(g - o) / max(np.linalg.norm(o), 1e-300))
+
+
+def _ragged(seed, nq, lq, lens, dim):
+    g = torch.Generator().manual_seed(seed)
+    lens = torch.tensor(lens, dtype=torch.int64)
+    off = synth.csr_offsets(lens)
+    Q = synth.unit_rows(nq * lq, dim, g, "cpu", torch.bfloat16).reshape(nq, lq, dim)
+    D = synth.unit_rows(int(off[-1]), dim, g, "cpu", torch.bfloat16)
+    return Q, D, off
+
+
+def _to_dev(*ts):
+    return [t.to(DEV) for t in ts]
+
+
+# ------------------------------------------------------------------------------ MaxSim scores
+
+def test_tiny_maxsim_scores_match_oracle():
+    w = synth.tiny_maxsim(seed=0)
+    Q, D, off = _to_dev(w["Q"], w["D"], w["off"])
+    S = hpr.maxsim_score(Q, D, off).cpu().numpy()
+    O = oracle.maxsim_scores(_bf(w["Q"]), _bf(w["D"]), w["off"].numpy())
+    _assert_close(S, O, what="scores")
+    _assert_close(S, O, rel=1e-4, what="scores (tight)")
+    # quantisation effect of rounding the fp32 tokens to bf16, reported against the fp32 oracle
+    O32 = oracle.maxsim_scores(w["Q_f32"].numpy().astype(np.float64),
+                               w["D_f32"].numpy().astype(np.float64), w["off"].numpy())
+    _assert_close(S, O32, what="scores vs fp32-token oracle")
+
+
+@pytest.mark.parametrize("nq,lq,lens,dim", [
+    (1, 1, [1], 8),
+    (3, 1, [1, 2, 3, 16, 17], 16),
+    (2, 3, [5, 1, 31, 32, 33], 64),
+    (5, 17, [15, 16, 17, 100, 1, 300], 128),
+    (9, 32, [513, 7, 64, 200], 128),
+    (4, 100, [40, 41], 96),
+    (3, 128, [20, 260, 3], 128),
+    (6, 64, [33, 1, 90], 256),
+    (2, 33, [50, 17], 192),
+    (17, 8, list(range(1, 40)), 32),
+])
+def test_maxsim_scores_edge_shapes(nq, lq, lens, dim):
+    Q, D, off = _ragged(100 + nq + lq + dim, nq, lq, lens, dim)
+    S = hpr.maxsim_score(*_to_dev(Q, D, off)).cpu().numpy()
+    O = oracle.maxsim_scores(_bf(Q), _bf(D), off.numpy())
+    _assert_close(S, O, what="scores")
+    _assert_close(S, O, rel=1e-4, what="scores (tight)")
+
+
+def test_maxsim_many_ranges_and_query_groups():
+    # enough documents and queries for several document ranges and query workgroups
+    g = torch.Generator().manual_seed(7)
+    lens = torch.randint(1, 200, (3000,), generator=g)
+    Q, D, off = _ragged(8, 70, 32, lens.tolist(), 128)
+    S = hpr.maxsim_score(*_to_dev(Q, D, off)).cpu().numpy()
+    O = oracle.maxsim_scores(_bf(Q), _bf(D), off.numpy())
+    _assert_close(S, O, rel=1e-4, what="scores")
+
+
+def test_maxsim_document_token_order_is_bit_invariant():
+    Q, D, off = _ragged(21, 6, 32, [70, 33, 128], 128)
+    S1 = hpr.maxsim_score(*_to_dev(Q, D, off))
+    perm = torch.cat([torch.randperm(int(off[d + 1] - off[d]),
+                                     generator=torch.Generator().manual_seed(d)) + off[d]
+                      for d in range(3)])
+    S2 = hpr.maxsim_score(*_to_dev(Q, D[perm].contiguous(), off))
+    S3 = hpr.maxsim_score(*_to_dev(Q, D, off))
+    assert torch.equal(S1, S2), "permuting a document's tokens changed its score bits"
+    assert torch.equal(S1, S3), "repeated call is not bit-identical"
+
+
+def test_maxsim_doc_equal_to_query_scores_sum_of_squared_norms():
+    Q, D, off = _ragged(22, 2, 32, [10], 128)
+    D = torch.cat([Q[0], D, Q[1][:5]])        # doc 0 = query 0's tokens; doc 1 = noise + part of q1
+    off = torch.tensor([0, 32, 32 + 15], dtype=torch.int64)
+    S = hpr.maxsim_score(*_to_dev(Q, D, off)).cpu().numpy()
+    q0 = _bf(Q[0])
+    want = float(np.sum(q0 * q0))
+    assert abs(S[0, 0] - want) <= 1e-4 * want
+    assert abs(want - 32) < 32 * 2 ** -6
+
+
+# ------------------------------------------------------------------------------ top-k
+
+def test_tiny_maxsim_topk():
+    w = synth.tiny_maxsim(seed=0)
+    s, i = hpr.maxsim_topk(*_to_dev(w["Q"], w["D"], w["off"]), w["k"])
+    O = oracle.maxsim_scores(_bf(w["Q"]), _bf(w["D"]), w["off"].numpy())
+    s, i = s.cpu().numpy(), i.cpu().numpy()
+    exact = 0
+    for q in range(O.shape[0]):
+        r = check_topk(s[q], i[q], O[q], w["k"])
+        exact += r["exact"]
+    assert exact == O.shape[0]
+
+
+@pytest.mark.parametrize("n_docs,k", [(1, 1), (7, 7), (300, 1), (300, 300), (2500, 1000),
+                                      (5000, 1024)])
+def test_maxsim_topk_edges(n_docs, k):
+    g = torch.Generator().manual_seed(n_docs + k)
+    lens = torch.randint(1, 40, (n_docs,), generator=g)
+    Q, D, off = _ragged(n_docs, 3, 8, lens.tolist(), 64)
+    s, i = hpr.maxsim_topk(*_to_dev(Q, D, off), k)
+    O = oracle.maxsim_scores(_bf(Q), _bf(D), off.numpy())
+    s, i = s.cpu().numpy(), i.cpu().numpy()
+    for q in range(3):
+        check_topk(s[q], i[q], O[q], k)
+
+
+def test_topk_duplicate_documents_lower_index_first():
+    Q, D, off = _ragged(31, 2, 16, [20, 30, 25], 128)
+    # docs 0, 2, 4 identical (bit-equal scores); docs 1, 3 other
+    toks = [D[0:20], D[20:50], D[0:20], D[50:75], D[0:20]]
+    D2 = torch.cat(toks)
+    off2 = synth.csr_offsets(torch.tensor([20, 30, 20, 25, 20]))
+    S = hpr.maxsim_score(*_to_dev(Q, D2, off2))
+    assert torch.equal(S[:, 0], S[:, 2]) and torch.equal(S[:, 0], S[:, 4])
+    s, i = hpr.maxsim_topk(*_to_dev(Q, D2, off2), 5)
+    for q in range(2):
+        pos = [int(x) for x in i[q].tolist()]
+        assert pos.index(0) < pos.index(2) < pos.index(4)
+        # exact order under (score desc, idx asc) using the GPU's own scores
+        Sq = S[q].cpu().numpy()
+        assert pos == sorted(range(5), key=lambda d: (-Sq[d], d))
+
+
+def test_topk_all_equal_scores_returns_lowest_indices():
+    Q, D, off = _ragged(32, 1, 4, [3], 32)
+    D2 = torch.cat([D] * 50)
+    off2 = synth.csr_offsets(torch.full((50,), 3))
+    s, i = hpr.maxsim_topk(*_to_dev(Q, D2, off2), 17)
+    assert i[0].tolist() == list(range(17))
+    assert torch.all(s[0] == s[0, 0])
+
+
+# ------------------------------------------------------------------------------ InfoNCE loss
+
+def _loss_parity(Q, D, off, pos, scale, rel_grad=REL):
+    r = hpr.coltrast_loss_fwd_bwd(*_to_dev(Q, D, off, pos), scale, return_scores=True)
+    o = oracle.coltrast_li_loss(_bf(Q), _bf(D), off.numpy(), pos.numpy(), scale)
+    _assert_close(r["scores"].cpu().numpy(), o["S"], rel=1e-4, what="scores")
+    _assert_close(r["loss"].cpu().numpy()[0], o["loss"], what="loss")
+    e_dq = _rel_l2(r["dq"].cpu().numpy(), o["dQ"])
+    e_dd = _rel_l2(r["dd"].cpu().numpy(), o["dD"])
+    assert e_dq <= rel_grad, f"dQ rel L2 {e_dq:.3g}"
+    assert e_dd <= rel_grad, f"dD rel L2 {e_dd:.3g}"
+    return r, o
+
+
+@pytest.mark.parametrize("scale", [50.0, 1.5625])
+def test_coltrast_step_loss_and_grads(scale):
+    w = synth.coltrast_step(seed=0)
+    r, o = _loss_parity(w["Q"], w["D"], w["off"], w["pos"], scale)
+    if scale == 1.5625:
+        assert abs(o["loss"] - 0.6385) < 0.01   # the recipe's expected magnitude
+    # rows the oracle's argmax never selects are zero on the GPU too, except where a near-tie
+    # (within fp32 rounding of the two dot products) sent the selection to another token
+    zero_rows = ~np.any(o["dD"] != 0, axis=1)
+    assert zero_rows.any()
+    g_rows = r["dd"].cpu().numpy()[zero_rows]
+    moved = np.any(g_rows != 0, axis=1)
+    assert moved.sum() <= 1e-3 * zero_rows.sum(), f"{moved.sum()} unselected rows non-zero"
+    assert np.linalg.norm(g_rows) <= 2e-3 * np.linalg.norm(o["dD"])
+
+
+@pytest.mark.parametrize("nq,lq,lens,dim,scale", [
+    (1, 1, [1, 1], 8, 1.0),
+    (3, 5, [4, 9, 1, 17], 16, 2.0),
+    (4, 17, [33, 16, 5, 70, 8], 64, 0.7),
+    (6, 32, [100, 1, 47, 256, 300, 12, 64], 128, 10.0),
+    (2, 40, [20, 21, 22], 256, 3.0),
+])
+def test_loss_small_shapes(nq, lq, lens, dim, scale):
+    Q, D, off = _ragged(nq * 7 + lq, nq, lq, lens, dim)
+    g = torch.Generator().manual_seed(nq)
+    pos = torch.randint(0, len(lens), (nq,), generator=g, dtype=torch.int32)
+    _loss_parity(Q, D, off, pos, scale)
+
+
+def test_loss_grads_optional_and_deterministic():
+    w = synth.coltrast_step(seed=1, nq=8, n_neg=3, ld=64)
+    args = _to_dev(w["Q"], w["D"], w["off"], w["pos"])
+    full = hpr.coltrast_loss_fwd_bwd(*args, 1.5625)
+    again = hpr.coltrast_loss_fwd_bwd(*args, 1.5625)
+    for key in ("loss", "dq", "dd"):
+        assert torch.equal(full[key], again[key]), f"{key} not bit-reproducible"
+    only_q = hpr.coltrast_loss_fwd_bwd(*args, 1.5625, need_dd=False)
+    only_d = hpr.coltrast_loss_fwd_bwd(*args, 1.5625, need_dq=False)
+    assert only_q["dd"] is None and only_d["dq"] is None
+    assert torch.equal(only_q["dq"], full["dq"]) and torch.equal(only_d["dd"], full["dd"])
+    assert torch.equal(only_q["loss"], full["loss"])
+
+
+def test_loss_bad_positive_gives_nan():
+    w = synth.coltrast_step(seed=2, nq=4, n_neg=1, ld=32)
+    pos = w["pos"].clone()
+    pos[1] = 10_000
+    r = hpr.coltrast_loss_fwd_bwd(*_to_dev(w["Q"], w["D"], w["off"], pos), 1.0)
+    assert math.isnan(float(r["loss"].item()))
+
+
+def test_autograd_function_matches_fwd_bwd_and_scales():
+    w = synth.coltrast_step(seed=3, nq=4, n_neg=3, ld=32)
+    Q = w["Q"].to(DEV).requires_grad_(True)
+    D = w["D"].to(DEV).requires_grad_(True)
+    off, pos = _to_dev(w["off"], w["pos"])
+    loss = hpr.coltrast_loss(Q, D, off, pos, 1.5625)
+    (3.0 * loss).backward()
+    ref = hpr.coltrast_loss_fwd_bwd(Q.detach(), D.detach(), off, pos, 1.5625)
+    assert torch.allclose(Q.grad.float(), (3.0 * ref["dq"]).bfloat16().float())
+    assert torch.allclose(D.grad.float(), (3.0 * ref["dd"]).bfloat16().float())
+    assert float(loss) == float(ref["loss"][0])
+
+
+# ------------------------------------------------------------------------------ plumbing
+
+def test_calls_on_a_non_default_stream():
+    w = synth.tiny_maxsim(seed=4)
+    Q, D, off = _to_dev(w["Q"], w["D"], w["off"])
+    ref = hpr.maxsim_score(Q, D, off)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        out = hpr.maxsim_score(Q, D, off)
+    s.synchronize()
+    assert torch.equal(ref, out)
+
+
+def test_csr_validate():
+    good = torch.tensor([0, 3, 4, 9], dtype=torch.int64, device=DEV)
+    assert hpr.csr_validate(good, 9) == ("HPR_OK", -1)
+    empty = torch.tensor([0, 3, 3, 9], dtype=torch.int64, device=DEV)
+    assert hpr.csr_validate(empty, 9) == ("HPR_ERR_EMPTY_DOC", 1)
+    dec = torch.tensor([0, 5, 4, 9], dtype=torch.int64, device=DEV)
+    assert hpr.csr_validate(dec, 9) == ("HPR_ERR_BAD_CSR", 1)
+    end = torch.tensor([0, 5, 8], dtype=torch.int64, device=DEV)
+    assert hpr.csr_validate(end, 9) == ("HPR_ERR_BAD_CSR", 1)
+    start = torch.tensor([1, 5, 9], dtype=torch.int64, device=DEV)
+    assert hpr.csr_validate(start, 9) == ("HPR_ERR_BAD_CSR", 0)
+
+
+def test_loss_call_replays_correctly_in_a_hip_graph():
+    # every library launch of the call is captured; replays with eager work and synchronisation
+    # in between must reproduce the eager result bit for bit each time
+    w = synth.coltrast_step(seed=5, nq=16, n_neg=7, ld=64)
+    Q, D, off, pos = _to_dev(w["Q"], w["D"], w["off"], w["pos"])
+    ws = hpr.coltrast_workspace(Q, D, off)
+    out = {"loss": torch.empty(1, device=DEV), "dq": torch.empty(Q.shape, device=DEV),
+           "dd": torch.empty(D.shape, device=DEV)}
+    eager = hpr.coltrast_loss_fwd_bwd(Q, D, off, pos, 1.5625)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        hpr.coltrast_loss_fwd_bwd(Q, D, off, pos, 1.5625, ws=ws, out=out)
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        hpr.coltrast_loss_fwd_bwd(Q, D, off, pos, 1.5625, ws=ws, out=out)
+    for rep in range(4):
+        for key in ("loss", "dq", "dd"):
+            out[key].fill_(float("nan"))
+        g.replay()
+        hpr.maxsim_score(Q, D, off)             # unrelated eager work between replays
+        torch.cuda.synchronize()
+        for key in ("loss", "dq", "dd"):
+            assert torch.equal(out[key], eager[key]), f"replay {rep}: {key} differs"
+
+
+def test_topk_call_replays_correctly_in_a_hip_graph():
+    w = synth.tiny_maxsim(seed=6)
+    Q, D, off = _to_dev(w["Q"], w["D"], w["off"])
+    ref_s, ref_i = hpr.maxsim_topk(Q, D, off, 10)
+    ws = torch.empty(hpr.lib().maxsim_topk_workspace_size(8, 32, 256, D.shape[0], 128, 10),
+                     dtype=torch.uint8, device=DEV)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        hpr.maxsim_topk(Q, D, off, 10, ws=ws)
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        s, i = hpr.maxsim_topk(Q, D, off, 10, ws=ws)
+    for rep in range(3):
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(s, ref_s) and torch.equal(i, ref_i), f"replay {rep}"
