@@ -44,9 +44,16 @@ COMMON_FLAGS = [
 ]
 
 
+# Per-file extra flags.  The MaxSim kernels take inputs that are finite by contract (the header
+# states it), so NaN semantics need not be honoured there: without this every fmaxf of the
+# running max is preceded by two NaN-quieting self-maxes, tripling the VALU work per tile.
+FILE_FLAGS = {"maxsim.hip": ["-fno-honor-nans"]}
+
+
 def _compile(src, verbose):
     obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
-    cmd = [_hipcc(), *COMMON_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [_hipcc(), *COMMON_FLAGS, *FILE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src),
+           "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     errs = "\n".join(l for l in (r.stderr or "").splitlines() if "packed-fp32-ops" not in l)
     if r.returncode != 0:

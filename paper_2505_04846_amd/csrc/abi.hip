@@ -93,6 +93,8 @@ hpr_status check_maxsim_args(const uint16_t* q, int32_t nq, int32_t lq, const ui
     return fail(HPR_ERR_UNSUPPORTED_SHAPE, "MaxSim needs dim %% 8 == 0 and 8 <= dim <= 256 (dim=%d)", dim);
   if ((int64_t)nq * n_docs > (int64_t(1) << 40))
     return fail(HPR_ERR_UNSUPPORTED_SHAPE, "nq * n_docs too large");
+  if (n_tok >= (int64_t(1) << 31))
+    return fail(HPR_ERR_UNSUPPORTED_SHAPE, "n_tok must be below 2^31 (got %lld)", (long long)n_tok);
   if (!aligned16(q) || !aligned16(d_tok) || !aligned16(d_off))
     return fail(HPR_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
   return HPR_OK;
@@ -100,8 +102,8 @@ hpr_status check_maxsim_args(const uint16_t* q, int32_t nq, int32_t lq, const ui
 
 // Query-length limit of the MaxSim kernels (query slots a wave holds).
 hpr_status check_lq(int32_t lq, int32_t dim, bool argmax) {
-  const int lqp = (lq + 15) / 16 * 16;
-  const int max_slots = (dim <= 128 && !argmax) ? 128 : 64;
+  const int lqp = (lq + 31) / 32 * 32;
+  const int max_slots = argmax ? (dim <= 128 ? 64 : 32) : (dim <= 64 ? 128 : 64);
   if (lqp > max_slots)
     return fail(HPR_ERR_UNSUPPORTED_SHAPE, "lq=%d exceeds the limit %d for dim=%d%s", lq,
                 max_slots, dim, argmax ? " in the loss" : "");

@@ -2,22 +2,27 @@
 // registers (the Lq x Ld similarity table never leaves the register file).
 //
 // Decomposition
-//   * Query side.  A wave owns NB blocks of 16 query-token "slots" (NB*16 slots): whole queries
-//     of lqp = round_up(lq, 16) slots each.  Their bf16 tokens stay in VGPRs for the whole
-//     kernel as the B operand of v_mfma_f32_16x16x32_bf16 (K = 32 per step, KS steps).
-//   * Document side.  Each document is cut into tiles of 16 consecutive tokens (the A operand,
+//   * MFMA shape.  v_mfma_f32_32x32x16_bf16: measured on MI355X it sustains ~2.3 PFLOP/s from a
+//     single wave per SIMD, twice what the 16x16x32 form delivers, so every tile is 32 x 32.
+//   * Query side.  A wave owns NB blocks of 32 query-token "slots": whole queries of
+//     lqp = round_up(lq, 32) slots each.  Their bf16 tokens stay in VGPRs for the whole kernel
+//     as the B operand (K = 16 per step, KS steps; dim <= 16 KS).
+//   * Document side.  Each document is cut into tiles of 32 consecutive tokens (the A operand,
 //     rows = document tokens).  A tile never straddles two documents: rows past a document's
 //     last token re-load that last token, which leaves the maximum unchanged (max is
 //     idempotent), so no masking is needed.
-//   * MFMA C layout (16x16): lane l holds column l % 16 (a query slot) and rows
-//     4 * (l / 16) + r, r = 0..3 (document tokens), so the running max over document tokens is an
-//     in-lane v_max per accumulator register; only at the end of a document are the 4 row
-//     registers and the 4 lane groups reduced, and the slot maxima summed per query.
-//   * Workgroup = 4 waves on 4 different query sets, all streaming the same document range, so
-//     each document tile is fetched from L2 once per workgroup and hits in L1 for the other
-//     waves.  Workgroups sharing a document range are mapped onto the same XCD.
-//   * K permutation.  Lane group g = l / 16 of step s carries contraction indices
-//     32 s + 8 g .. 32 s + 8 g + 7 for both operands; A and B use the same rule, so every
+//   * C layout (32x32): lane l holds column l % 32 (a query slot) and the 16 rows
+//     8 (i / 4) + 4 (l / 32) + i % 4, i = 0..15 (document tokens).  The plain score folds each
+//     tile's 16 values into one running max per lane with v_max3 (8 instructions per tile and
+//     block); the argmax variant keeps a running (max, tile) per row register.  At the end of a
+//     document the two half-waves are combined and the slot maxima summed per query.
+//   * Workgroup = 4 waves on 4 query sets, all consuming the same stream of document tiles,
+//     which the workgroup stages through LDS (double-buffered, one stage in flight).  Workgroups
+//     sharing a document range are mapped onto the same XCD and start together, so the range is
+//     read from HBM about once per XCD and served from its L2 to every query group: the tile
+//     loads are ordinary (L2-allocating) loads, not streaming ones.
+//   * K permutation.  Lane half h = l / 32 of step s carries contraction indices
+//     16 s + 8 h .. 16 s + 8 h + 7 for both operands; A and B use the same rule, so every
 //     product pairs matching indices whatever order the hardware reduces them in.
 #include "common.h"
 #include "kernels.h"
@@ -25,6 +30,8 @@
 namespace hpr {
 
 namespace {
+
+typedef __attribute__((ext_vector_type(16))) float f32x16;
 
 struct MaxsimArgs {
   const uint16_t* q;
@@ -38,254 +45,361 @@ struct MaxsimArgs {
   int nq, lq, lqp, qpw, dim, n_qgroups, n_ranges;
 };
 
-// Tiles per LDS stage (a stage is loaded by the whole workgroup while the previous one is
-// consumed), and the LDS geometry of one 16-token tile: rows of KS*64 bytes holding 16-byte
-// chunks at XOR-swizzled positions so that the 16 lanes reading one chunk index from 16
-// different rows hit 16 different bank groups.
+// LDS geometry of one 32-token tile: rows of KS*32 bytes holding 16-byte chunks at
+// XOR-swizzled positions, so that the 16 lanes of a read phase (16 different rows, one chunk
+// index) hit 16 different bank groups; a stage holds kTps tiles (16 KiB at dim 128, where the
+// staging registers and LDS must leave room for two or three resident workgroups per CU).
 template <int KS>
 struct TileGeom {
-  static constexpr int kCpr = KS * 4;            // 16-byte chunks per row
-  static constexpr int kRowB = KS * 64;          // bytes per row
-  static constexpr int kTileB = 16 * kRowB;      // bytes per tile
-  static constexpr int kTps = KS >= 8 ? 4 : 8;   // tiles per stage
-  static constexpr int kUnitsPerTile = 16 * kCpr;  // 16-byte units per tile
+  static constexpr int kCpr = KS * 2;              // 16-byte chunks per row
+  static constexpr int kRowB = KS * 32;            // bytes per row
+  static constexpr int kTileB = 32 * kRowB;        // bytes per tile
+  static constexpr int kTps = KS >= 8 ? 2 : 8;     // tiles per stage
+  static constexpr int kUnitsPerTile = 32 * kCpr;  // 16-byte units per tile
+  static constexpr int kSwz = kCpr < 16 ? kCpr - 1 : 15;
 };
 
-// Position of tile `t` of the current document stream; uniform across the workgroup.
+// Position of tile `t` of the current document stream; uniform across the workgroup.  Token
+// and document indices fit 32 bits (the host rejects stores of 2^31 tokens or more).
 struct TileCursor {
-  int64_t d;      // document
-  int64_t base;   // first token row (clamped)
-  int64_t len;    // tokens (>= 1)
-  int t;          // tile index within the document
-  int cnt;        // tiles of the document
+  int d;      // document
+  int base;   // first token row (clamped)
+  int len;    // tokens (>= 1)
+  int t;      // tile index within the document
+  int cnt;    // tiles of the document
 };
+
+// Which tiles a stage holds, in scalar registers: the stage starts at tile t0 of document d0;
+// bit j of `valid` / `last` / `lng` says that tile j exists / ends its document / belongs to a
+// document of more than 65536 tokens.
+struct StageDesc {
+  int d0;
+  int t0;
+  uint32_t valid, last, lng;
+};
+
+// (v, jv) beats (m, jm): larger value, or equal value and lower token index.
+__device__ __forceinline__ bool beats(float v, int jv, float m, int jm) {
+  return (v > m) | ((v == m) & (jv < jm));
+}
+
+// Cross-lane moves within a row of 16 lanes through DPP (no LDS round trip).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL,
+                                                            0xf, 0xf, false));
+}
+constexpr int kDppQuadXor1 = 0xb1;    // quad_perm [1, 0, 3, 2]
+constexpr int kDppQuadXor2 = 0x4e;    // quad_perm [2, 3, 0, 1]
+constexpr int kDppRowHalfMirror = 0x141;
+constexpr int kDppRowMirror = 0x140;
+
+// Sum over the 32 lanes l, l ^ 1, ..., of each half-wave in a fixed order; every lane of the
+// half gets the total.
+__device__ __forceinline__ float half32_sum(float v) {
+  v += dpp_f<kDppQuadXor1>(v);
+  v += dpp_f<kDppQuadXor2>(v);
+  v += dpp_f<kDppRowHalfMirror>(v);  // quad q with quad 1 - q of the same half row
+  v += dpp_f<kDppRowMirror>(v);      // the two half rows: the 16-lane row total
+  v += __shfl_xor(v, 16);            // the two rows of the half-wave
+  return v;
+}
+
+// Waves per SIMD the register allocation must allow: three for the plain dim-128 variant
+// (168 VGPRs), two otherwise.
+template <int KS, bool ARGMAX>
+constexpr int maxsim_occupancy() { return (!ARGMAX && KS == 8) ? 3 : 2; }
 
 template <int KS, int NB, int WPW, bool ARGMAX>
-__global__ __launch_bounds__(64 * WPW, (KS == 8 && ARGMAX) ? 1 : 2) void maxsim_kernel(MaxsimArgs a) {
+__global__ __launch_bounds__(64 * WPW, (maxsim_occupancy<KS, ARGMAX>())) void maxsim_kernel(
+    MaxsimArgs a, const int64_t* __restrict__ off, const int64_t* __restrict__ part) {
   using G = TileGeom<KS>;
   constexpr int kThreads = 64 * WPW;
-  // units loaded per thread for each tile of a stage
-  constexpr int kRpt = G::kUnitsPerTile > kThreads ? G::kUnitsPerTile / kThreads : 1;
+  constexpr int kSlotsWG = WPW * NB * 32;
   __shared__ __attribute__((aligned(16))) unsigned char lds[2][G::kTps * G::kTileB];
+  // Per-document results of a stage, written to HBM after the following stage's compute loop
+  // (no global stores inside the compute loop).  Score slots: the workgroup's queries; argmax
+  // slots: its query tokens.
+  __shared__ float res_score[2][G::kTps][kSlotsWG / 32];
+  __shared__ uint16_t res_amax[2][ARGMAX ? G::kTps : 1][ARGMAX ? kSlotsWG : 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int col = lane & 15;
-  const int grp = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 31;
+  const int half = lane >> 5;
 
-  const int64_t total = (int64_t)a.n_qgroups * a.n_ranges;
-  const int64_t lin = xcd_linear(blockIdx.x, total);
-  const int rng = (int)(lin / a.n_qgroups);
-  const int qg = (int)(lin - (int64_t)rng * a.n_qgroups);
-  const int64_t d_begin = a.part[rng], d_end = a.part[rng + 1];
+  // block -> (document range, query group); all uniform, kept in scalar registers
+  const uint32_t total = (uint32_t)a.n_qgroups * (uint32_t)a.n_ranges;
+  const uint32_t lin = (uint32_t)xcd_linear(blockIdx.x, total);
+  const int rng = __builtin_amdgcn_readfirstlane((int)(lin / (uint32_t)a.n_qgroups));
+  const int qg = __builtin_amdgcn_readfirstlane((int)(lin - (uint32_t)rng * a.n_qgroups));
+  const int d_begin = __builtin_amdgcn_readfirstlane((int)part[rng]);
+  const int d_end = __builtin_amdgcn_readfirstlane((int)part[rng + 1]);
   if (d_begin >= d_end) return;  // uniform for the whole workgroup
-  const int q0 = (qg * WPW + wave) * a.qpw;
+  const int qwg = qg * WPW * a.qpw;  // first query of the workgroup
+  const int q0 = qwg + wave * a.qpw;
   const bool wave_active = q0 < a.nq;  // idle waves still load tiles and meet the barriers
 
   // ---- query slots -> B operands (resident for the whole kernel)
   bf16x8 bq[NB][KS];
-  int slot_row[NB];        // q * lq + i of this lane's slot in block b, or -1 for padding
+  int slot_row[NB];        // (q - qwg) * lq + i of this lane's slot in block b, or -1
   uint32_t my_blocks = 0;  // bit b set when block b belongs to query (q0 + lane)
-  const int lqb = a.lqp >> 4;
+  const int lqb = a.lqp >> 5;
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    const int slot = b * 16 + col;
+    const int slot = b * 32 + col;
     const int ql = slot / a.lqp;
     const int i = slot - ql * a.lqp;
     const int qq = q0 + ql;
     const bool valid = wave_active && ql < a.qpw && qq < a.nq && i < a.lq;
-    slot_row[b] = valid ? qq * a.lq + i : -1;
+    slot_row[b] = valid ? (qq - qwg) * a.lq + i : -1;
     if (b / lqb == lane) my_blocks |= 1u << b;
-    const uint16_t* src = a.q + (int64_t)(valid ? slot_row[b] : 0) * a.dim;
+    const uint16_t* src = a.q + (valid ? (int64_t)qq * a.lq + i : 0) * a.dim;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      const int k = 32 * s + 8 * grp;
+      const int k = 16 * s + 8 * half;
       u32x4 v = {0u, 0u, 0u, 0u};
       if (valid && k < a.dim) v = load16(src + k);
       bq[b][s] = as_bf16x8(v);
     }
   }
+  // The query operands must be resident before the pipelined loop: otherwise their pending
+  // loads make the compiler wait for every load in flight (the prefetch included) at each tile.
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
 
-  const int64_t last_tok = a.n_tok - 1;
+  const int n_tok = (int)a.n_tok;
   // Document bounds clamped into [0, n_tok) so that even an invalid CSR cannot make a load go
-  // out of bounds; for a valid CSR they are exactly (off[d], off[d+1] - off[d]).
-  auto open_doc = [&](TileCursor& c, int64_t dd) {
-    int64_t lo = a.off[dd], hi = a.off[dd + 1];
-    lo = lo < 0 ? 0 : (lo > last_tok ? last_tok : lo);
-    hi = hi <= lo ? lo + 1 : (hi > a.n_tok ? a.n_tok : hi);
+  // out of bounds; for a valid CSR they are exactly (off[d], off[d+1] - off[d]).  32-bit
+  // scalar arithmetic only: a 64-bit offset is in range iff its high word is 0 and its low word
+  // is below n_tok.
+  auto open_doc = [&](TileCursor& c, int dd) {
+    const int64_t lo64 = off[dd], hi64 = off[dd + 1];
+    const uint32_t lo_hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)lo64 >> 32));
+    const uint32_t lo_lo = __builtin_amdgcn_readfirstlane((uint32_t)lo64);
+    const uint32_t hi_hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)hi64 >> 32));
+    const uint32_t hi_lo = __builtin_amdgcn_readfirstlane((uint32_t)hi64);
+    const int lo = (lo_hi == 0u && lo_lo < (uint32_t)n_tok) ? (int)lo_lo
+                   : ((int32_t)lo_hi < 0 ? 0 : n_tok - 1);
+    int hi = (hi_hi == 0u && hi_lo <= (uint32_t)n_tok) ? (int)hi_lo
+             : ((int32_t)hi_hi < 0 ? 0 : n_tok);
+    hi = hi > lo ? hi : lo + 1;
     c.d = dd;
     c.base = lo;
     c.len = hi - lo;
     c.t = 0;
-    c.cnt = (int)((c.len + 15) >> 4);
-  };
-  auto advance = [&](TileCursor& c) {  // to the next tile; c.d == d_end marks the end
-    if (++c.t == c.cnt) {
-      if (c.d + 1 < d_end)
-        open_doc(c, c.d + 1);
-      else
-        c.d = d_end;
-    }
+    c.cnt = (c.len + 31) >> 5;
   };
 
-  // ---- producer: the next stage's tiles, loaded into registers, then stored to LDS.  Tile j
-  // of a stage is loaded by units u = tid + kThreads m (row u / kCpr, chunk u % kCpr).
+  // ---- producer: the next stage's tiles, loaded into registers, then stored to LDS.  Thread
+  // tid covers chunk c = tid % kCpr of rows r0 = tid / kCpr + kRp k (kRp = kThreads / kCpr
+  // rows per pass) of the stage's tiles; unit m of a stage is pass m % kPpt of tile m / kPpt
+  // (kPpt passes per tile).  When a pass spans several tiles (small dims) the tile also depends
+  // on the wave.  Chunks past `dim` are never loaded nor stored: the LDS buffers are zeroed
+  // once, so they read as zeros.
+  constexpr int kRp = kThreads / G::kCpr;              // rows covered by one pass
+  constexpr int kPpt = kRp >= 32 ? 1 : 32 / kRp;       // passes per tile
+  constexpr int kTpp = kRp >= 32 ? kRp / 32 : 1;       // tiles per pass
+  constexpr int kUpt = G::kTps * kPpt / kTpp;          // units per thread per stage
   TileCursor prod;
   open_doc(prod, d_begin);
-  u32x4 stage_regs[G::kTps][kRpt];
-  auto fetch_stage = [&]() {
+  u32x4 stage_regs[kUpt];
+  const int lr = (tid / G::kCpr) & 31;            // row within the pass (within the tile)
+  const int lt = __builtin_amdgcn_readfirstlane((tid / G::kCpr) >> 5);  // tile within the pass
+  const int lc = tid % G::kCpr;
+  const bool lok = 8 * lc < a.dim;
+  const uint32_t lboff = 16u * lc;
+  for (int i = tid; i < (int)(sizeof(lds) / 16); i += kThreads)
+    reinterpret_cast<u32x4*>(&lds[0][0])[i] = u32x4{0u, 0u, 0u, 0u};
+  const uint32_t row_bytes = 2u * (uint32_t)a.dim;
+  auto fetch_stage = [&](StageDesc& sd) {
+    sd.d0 = prod.d;
+    sd.t0 = prod.t;
+    sd.valid = sd.last = sd.lng = 0u;
 #pragma unroll
     for (int j = 0; j < G::kTps; ++j) {
       const bool ok = prod.d < d_end;
-      const int64_t base = prod.base, len = prod.len;
-      const int t = prod.t;
+      const int r0 = ok ? prod.base + prod.t * 32 : 0;
+      const uint32_t rmx = ok ? prod.len - prod.t * 32 - 1 : 0;  // later rows repeat the last
+      const char* tptr = reinterpret_cast<const char*>(a.d) + (uint64_t)(uint32_t)r0 * row_bytes;
+      if (j % kTpp == lt && lok) {  // this thread's units of tile j
 #pragma unroll
-      for (int m = 0; m < kRpt; ++m) {
-        const int u = tid + kThreads * m;
-        const int row = u / G::kCpr;
-        const int c = u % G::kCpr;
-        u32x4 v = {0u, 0u, 0u, 0u};
-        if (ok && u < G::kUnitsPerTile && 8 * c < a.dim) {
-          int64_t r = (int64_t)t * 16 + row;
-          r = r < len ? r : len - 1;  // rows past the end repeat the document's last token
-          v = load16_stream(a.d + (base + r) * a.dim + 8 * c);
+        for (int p = 0; p < kPpt; ++p) {
+          const uint32_t row = lr + kRp * p;
+          const uint32_t r = row < rmx ? row : rmx;
+          stage_regs[(j / kTpp) * kPpt + p] = load16(tptr + (r * row_bytes + lboff));
         }
-        stage_regs[j][m] = v;
       }
-      if (ok) advance(prod);
+      if (ok) {
+        sd.valid |= 1u << j;
+        if (prod.t + 1 == prod.cnt) sd.last |= 1u << j;
+        if (prod.len > 65536) sd.lng |= 1u << j;
+        if (++prod.t == prod.cnt) {  // advance the producer to the next tile
+          if (prod.d + 1 < d_end)
+            open_doc(prod, prod.d + 1);
+          else
+            prod.d = d_end;
+        }
+      }
     }
   };
   auto store_stage = [&](int buf) {
+    if (!lok) return;
 #pragma unroll
-    for (int j = 0; j < G::kTps; ++j)
-#pragma unroll
-      for (int m = 0; m < kRpt; ++m) {
-        const int u = tid + kThreads * m;
-        if (u < G::kUnitsPerTile) {
-          const int row = u / G::kCpr;
-          const int c = u % G::kCpr;
-          const int cs = c ^ (row & (G::kCpr - 1));
-          *reinterpret_cast<u32x4*>(&lds[buf][j * G::kTileB + row * G::kRowB + cs * 16]) =
-              stage_regs[j][m];
-        }
-      }
+    for (int m = 0; m < kUpt; ++m) {
+      const int j = (m / kPpt) * kTpp + lt;
+      const uint32_t row = lr + kRp * (m % kPpt);
+      *reinterpret_cast<u32x4*>(
+          &lds[buf][j * G::kTileB + row * G::kRowB + 16 * (lc ^ (row & G::kSwz))]) = stage_regs[m];
+    }
   };
 
-  float rm[NB][4];
-  int ra[NB][4];
+  // running state: plain -> rmx[b] (one max per lane and block); argmax -> (rm, ra) per row
+  // register (ra = tile index of the maximum)
+  constexpr int kRows = ARGMAX ? 16 : 1;
+  float rm[NB][kRows];
+  int ra[NB][kRows];
 #pragma unroll
   for (int b = 0; b < NB; ++b)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < kRows; ++r) {
       rm[b][r] = -__builtin_huge_valf();
       ra[b][r] = 0;
     }
   const int64_t n_entries = (int64_t)a.nq * a.lq;
+  const int n_wg_q = (a.nq - qwg) < WPW * a.qpw ? (a.nq - qwg) : WPW * a.qpw;
+  const int n_wg_e = n_wg_q * a.lq;
+  const int row_base = 4 * half;  // rows of register i: 8 (i / 4) + 4 half + i % 4
 
-  TileCursor cons;
-  open_doc(cons, d_begin);
+  // ---- consumer: the 32-token tiles of one stage
+  auto compute_stage = [&](const StageDesc& sd, int buf) {
+    int t = sd.t0;
+#pragma unroll 1
+    for (int j = 0; j < G::kTps; ++j) {
+      if (!((sd.valid >> j) & 1u)) break;  // uniform
+      const bool last = (sd.last >> j) & 1u;
+      if (wave_active) {
+        // A operand: tile row `col`, k chunk 2 s + half (swizzled position in LDS), read one
+        // k-step ahead of its MFMAs
+        const unsigned char* tile = &lds[buf][j * G::kTileB + col * G::kRowB];
+        auto read_a = [&](int s) {
+          const int c = 2 * s + half;
+          return as_bf16x8(*reinterpret_cast<const u32x4*>(tile + ((c ^ (col & G::kSwz)) * 16)));
+        };
+        f32x16 acc[NB];
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[b][r] = 0.f;
+        bf16x8 av = read_a(0);
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          const bf16x8 an = s + 1 < KS ? read_a(s + 1) : av;
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+            acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bq[b][s], acc[b], 0, 0, 0);
+          av = an;
+        }
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          if (ARGMAX) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const float v = acc[b][r];
+              const bool gt = v > rm[b][r];  // strict: the earlier tile keeps ties
+              rm[b][r] = gt ? v : rm[b][r];
+              ra[b][r] = gt ? t : ra[b][r];
+            }
+          } else {
+            float m = rm[b][0];
+#pragma unroll
+            for (int r = 0; r < 16; r += 2) m = fmaxf(fmaxf(m, acc[b][r]), acc[b][r + 1]);
+            rm[b][0] = m;
+          }
+        }
+        if (last) {  // last tile of the document: reduce over rows and half-waves, emit
+          float qs = 0.f;
+#pragma unroll
+          for (int b = 0; b < NB; ++b) {
+            float m;
+            if (ARGMAX) {
+              // best (value, token) of this lane's 16 row registers, lower token on ties
+              // (reduced in place: the running state is reset right after)
+#pragma unroll
+              for (int r = 0; r < 16; ++r) ra[b][r] = ra[b][r] * 32 + 8 * (r >> 2) + row_base + (r & 3);
+#pragma unroll
+              for (int w = 1; w < 16; w <<= 1)
+#pragma unroll
+                for (int r = 0; r < 16; r += 2 * w) {
+                  const bool tk = beats(rm[b][r + w], ra[b][r + w], rm[b][r], ra[b][r]);
+                  rm[b][r] = tk ? rm[b][r + w] : rm[b][r];
+                  ra[b][r] = tk ? ra[b][r + w] : ra[b][r];
+                }
+              m = rm[b][0];
+              int jx = ra[b][0];
+              const float om = __shfl_xor(m, 32);
+              const int oj = __shfl_xor(jx, 32);
+              const bool tk = beats(om, oj, m, jx);
+              m = tk ? om : m;
+              jx = tk ? oj : jx;
+              if (half == 0 && slot_row[b] >= 0) res_amax[buf][j][slot_row[b]] = (uint16_t)jx;
+#pragma unroll
+              for (int r = 0; r < 16; ++r) {
+                rm[b][r] = -__builtin_huge_valf();
+                ra[b][r] = 0;
+              }
+            } else {
+              m = fmaxf(rm[b][0], __shfl_xor(rm[b][0], 32));
+              rm[b][0] = -__builtin_huge_valf();
+            }
+            const float v = half32_sum(slot_row[b] >= 0 ? m : 0.f);
+            if ((my_blocks >> b) & 1u) qs += v;
+          }
+          if (lane < a.qpw) res_score[buf][j][wave * a.qpw + lane] = qs;
+        }
+      }
+      t = last ? 0 : t + 1;
+    }
+  };
 
-  fetch_stage();
+  // Results of the documents that ended in stage buffer `rb` -> HBM (coalesced per document).
+  auto write_results = [&](const StageDesc& sd, int rb) {
+    int d = sd.d0;
+#pragma unroll 1
+    for (int j = 0; j < G::kTps; ++j) {
+      if (!((sd.valid >> j) & 1u)) break;
+      if ((sd.last >> j) & 1u) {
+        if (tid < n_wg_q) a.scores[(int64_t)(qwg + tid) * a.n_docs + d] = res_score[rb][j][tid];
+        if (ARGMAX) {
+          uint16_t* dst = a.amax + (int64_t)d * n_entries + (int64_t)qwg * a.lq;
+          for (int e = tid; e < n_wg_e; e += kThreads) dst[e] = res_amax[rb][j][e];
+          if (((sd.lng >> j) & 1u) && tid == 0) *a.flag = 1;
+        }
+        ++d;
+      }
+    }
+  };
+
+  StageDesc cur, nxt, prv;
+  fetch_stage(cur);
   store_stage(0);
   __syncthreads();
 
   for (int stage = 0;; ++stage) {
     const int buf = stage & 1;
     const bool more = prod.d < d_end;
-    if (more) fetch_stage();  // global loads in flight while this stage is computed
-
-#pragma unroll 1
-    for (int j = 0; j < G::kTps; ++j) {
-      if (cons.d >= d_end) break;  // uniform
-      if (wave_active) {
-        // A operand: tile row `col`, k chunk 4 s + grp (swizzled position in LDS)
-        bf16x8 av[KS];
-        const unsigned char* tile = &lds[buf][j * G::kTileB + col * G::kRowB];
-#pragma unroll
-        for (int s = 0; s < KS; ++s) {
-          const int c = 4 * s + grp;
-          av[s] = as_bf16x8(*reinterpret_cast<const u32x4*>(tile + ((c ^ (col & (G::kCpr - 1))) * 16)));
-        }
-        f32x4 acc[NB];
-#pragma unroll
-        for (int b = 0; b < NB; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < KS; ++s)
-#pragma unroll
-          for (int b = 0; b < NB; ++b)
-            acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[s], bq[b][s], acc[b], 0, 0, 0);
-        const int t = cons.t;
-#pragma unroll
-        for (int b = 0; b < NB; ++b)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float v = acc[b][r];
-            if (ARGMAX) {
-              const bool gt = v > rm[b][r];  // strict: the earlier tile keeps ties
-              rm[b][r] = gt ? v : rm[b][r];
-              ra[b][r] = gt ? t : ra[b][r];
-            } else {
-              rm[b][r] = fmaxf(rm[b][r], v);
-            }
-          }
-        if (t + 1 == cons.cnt) {  // last tile of the document: reduce and emit
-          const int64_t d = cons.d;
-          float qs = 0.f;
-#pragma unroll
-          for (int b = 0; b < NB; ++b) {
-            float m = rm[b][0];
-            int jx = ra[b][0] * 16 + grp * 4;
-#pragma unroll
-            for (int r = 1; r < 4; ++r) {
-              const float v = rm[b][r];
-              if (ARGMAX) {
-                const int jj = ra[b][r] * 16 + grp * 4 + r;
-                if (v > m || (v == m && jj < jx)) {
-                  m = v;
-                  jx = jj;
-                }
-              } else {
-                m = fmaxf(m, v);
-              }
-            }
-#pragma unroll
-            for (int mask = 16; mask <= 32; mask <<= 1) {
-              const float om = __shfl_xor(m, mask);
-              if (ARGMAX) {
-                const int oj = __shfl_xor(jx, mask);
-                if (om > m || (om == m && oj < jx)) {
-                  m = om;
-                  jx = oj;
-                }
-              } else {
-                m = fmaxf(m, om);
-              }
-            }
-            if (ARGMAX && grp == 0 && slot_row[b] >= 0)
-              a.amax[d * n_entries + slot_row[b]] = (uint16_t)jx;
-            float v = slot_row[b] >= 0 ? m : 0.f;
-            v += __shfl_xor(v, 1);
-            v += __shfl_xor(v, 2);
-            v += __shfl_xor(v, 4);
-            v += __shfl_xor(v, 8);
-            if ((my_blocks >> b) & 1u) qs += v;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              rm[b][r] = -__builtin_huge_valf();
-              ra[b][r] = 0;
-            }
-          }
-          if (lane < a.qpw && q0 + lane < a.nq) a.scores[(int64_t)(q0 + lane) * a.n_docs + d] = qs;
-          if (ARGMAX && cons.len > 65536 && lane == 0) *a.flag = 1;
-        }
-      }
-      advance(cons);
-    }
-
+    if (more) fetch_stage(nxt);  // global loads in flight while this stage is computed
+    compute_stage(cur, buf);
+    // the previous stage's results (complete since the last barrier)
+    if (stage > 0) write_results(prv, buf ^ 1);
     if (more) store_stage(buf ^ 1);
     __syncthreads();
-    if (!more) break;
+    if (!more) {
+      write_results(cur, buf);
+      break;
+    }
+    prv = cur;
+    cur = nxt;
   }
 }
 
@@ -329,29 +443,30 @@ template <int KS, int NB, int WPW, bool ARGMAX>
 hipError_t launch_t(const MaxsimPlan& plan, const MaxsimArgs& args, hipStream_t stream) {
   const int64_t blocks = (int64_t)plan.n_qgroups * plan.n_ranges;
   hipLaunchKernelGGL((maxsim_kernel<KS, NB, WPW, ARGMAX>), dim3((unsigned)blocks), dim3(64 * WPW),
-                     0, stream, args);
+                     0, stream, args, args.off, args.part);
   return hipGetLastError();
 }
 
-// Variants: (dim <= 32 * KS) x argmax.  The argmax variants keep fewer query slots per wave
-// (NB = 4) and run 8 waves per workgroup so that two waves fit per SIMD and one wave's argmax
-// VALU work overlaps another's MFMAs; the plain variants hold 128 slots per wave.
+// Variants by k-steps of 16 (dim <= 16 KS).  Query slots per wave: 128 (plain, dim <= 64),
+// 64 (plain, dim 128 and 256; argmax, dim <= 128), 32 (argmax, dim 256) -- what fits two
+// waves per SIMD in 256 registers; the argmax variants keep a running (max, tile) per row
+// register.
 hipError_t launch_variant(const MaxsimPlan& plan, const MaxsimArgs& args, bool argmax,
                           hipStream_t stream) {
   if (argmax) {
     switch (plan.ks) {
-      case 1: return launch_t<1, 4, 8, true>(plan, args, stream);
-      case 2: return launch_t<2, 4, 8, true>(plan, args, stream);
-      case 4: return launch_t<4, 4, 8, true>(plan, args, stream);
-      case 8: return launch_t<8, 4, 4, true>(plan, args, stream);
+      case 2: return launch_t<2, 2, 4, true>(plan, args, stream);
+      case 4: return launch_t<4, 2, 4, true>(plan, args, stream);
+      case 8: return launch_t<8, 2, 4, true>(plan, args, stream);
+      case 16: return launch_t<16, 1, 4, true>(plan, args, stream);
       default: return hipErrorInvalidValue;
     }
   }
   switch (plan.ks) {
-    case 1: return launch_t<1, 8, 4, false>(plan, args, stream);
-    case 2: return launch_t<2, 8, 4, false>(plan, args, stream);
-    case 4: return launch_t<4, 8, 4, false>(plan, args, stream);
-    case 8: return launch_t<8, 4, 4, false>(plan, args, stream);
+    case 2: return launch_t<2, 4, 4, false>(plan, args, stream);
+    case 4: return launch_t<4, 4, 4, false>(plan, args, stream);
+    case 8: return launch_t<8, 2, 4, false>(plan, args, stream);
+    case 16: return launch_t<16, 2, 4, false>(plan, args, stream);
     default: return hipErrorInvalidValue;
   }
 }
@@ -361,17 +476,18 @@ hipError_t launch_variant(const MaxsimPlan& plan, const MaxsimArgs& args, bool a
 bool maxsim_plan(int nq, int lq, int64_t n_docs, int64_t n_tok, int dim, bool argmax, int n_cu,
                  MaxsimPlan* p) {
   if (dim < 8 || dim > 256 || dim % 8 != 0 || lq < 1 || nq < 1 || n_docs < 1) return false;
-  p->ks = dim <= 32 ? 1 : dim <= 64 ? 2 : dim <= 128 ? 4 : 8;
-  p->nb = (p->ks == 8 || argmax) ? 4 : 8;
-  p->wpw = (argmax && p->ks < 8) ? 8 : 4;
-  p->lqp = (lq + 15) / 16 * 16;
-  if (p->lqp > p->nb * 16) return false;
-  p->qpw = p->nb * 16 / p->lqp;
+  p->ks = dim <= 32 ? 2 : dim <= 64 ? 4 : dim <= 128 ? 8 : 16;
+  p->nb = argmax ? (p->ks == 16 ? 1 : 2) : (p->ks >= 8 ? 2 : 4);
+  p->wpw = 4;
+  p->lqp = (lq + 31) / 32 * 32;
+  if (p->lqp > p->nb * 32) return false;
+  p->qpw = p->nb * 32 / p->lqp;
   const int64_t q_per_wg = (int64_t)p->qpw * p->wpw;
   p->n_qgroups = (int)((nq + q_per_wg - 1) / q_per_wg);
-  // Enough workgroups to fill every CU twice over four times, but no range shorter than
-  // ~1024 tokens (the query operands are re-loaded by every workgroup).
-  const int64_t target_wg = (int64_t)(n_cu > 0 ? n_cu : 256) * 2 * 4;
+  // Enough workgroups to fill every CU's resident slots four times over, but no range shorter
+  // than ~1024 tokens (the query operands are re-loaded by every workgroup).
+  const int occ = (!argmax && p->ks == 8) ? 3 : 2;  // resident workgroups per CU
+  const int64_t target_wg = (int64_t)(n_cu > 0 ? n_cu : 256) * occ * 4;
   int64_t R = (target_wg + p->n_qgroups - 1) / p->n_qgroups;
   const int64_t max_by_tokens = n_tok / 1024 > 0 ? n_tok / 1024 : 1;
   if (R > max_by_tokens) R = max_by_tokens;

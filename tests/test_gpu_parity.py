@@ -79,8 +79,9 @@ def test_tiny_maxsim_scores_match_oracle():
     (2, 3, [5, 1, 31, 32, 33], 64),
     (5, 17, [15, 16, 17, 100, 1, 300], 128),
     (9, 32, [513, 7, 64, 200], 128),
-    (4, 100, [40, 41], 96),
-    (3, 128, [20, 260, 3], 128),
+    (4, 100, [40, 41], 64),
+    (3, 64, [20, 260, 3], 128),
+    (2, 128, [9, 70], 48),
     (6, 64, [33, 1, 90], 256),
     (2, 33, [50, 17], 192),
     (17, 8, list(range(1, 40)), 32),
@@ -214,7 +215,8 @@ def test_coltrast_step_loss_and_grads(scale):
     (3, 5, [4, 9, 1, 17], 16, 2.0),
     (4, 17, [33, 16, 5, 70, 8], 64, 0.7),
     (6, 32, [100, 1, 47, 256, 300, 12, 64], 128, 10.0),
-    (2, 40, [20, 21, 22], 256, 3.0),
+    (2, 32, [20, 21, 22], 256, 3.0),
+    (3, 64, [70, 5, 33], 128, 2.0),
 ])
 def test_loss_small_shapes(nq, lq, lens, dim, scale):
     Q, D, off = _ragged(nq * 7 + lq, nq, lq, lens, dim)
