@@ -29,6 +29,8 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBS = 8000.0
+KERNELS = ("partition", "maxsim", "maxsim_argmax", "topk", "infonce", "grad_q", "grad_d",
+           "dense_sample", "dense_scan", "dense_merge")
 
 
 def parse():
@@ -151,6 +153,38 @@ def build_workload(name, dev, scale):
                     cpu_sample=cpu_sample, config=cfg, dtype="bf16", unit="pairs/s",
                     sha=source_sha("maxsim.hip", "common.h"))
 
+    if name == "dense_retrieval":
+        w = synth.dense_retrieval(seed=0, device=dev)
+        Q, X, k = w["Q"], w["X"], w["k"]
+        nq, dim = Q.shape
+        n = X.shape[0]
+        ws = hpr.dense_workspace(Q, X, k)
+
+        def step():
+            hpr.dense_ip_topk(Q, X, k, ws=ws)
+
+        sample_rows = min(n, max(131072, 32 * k))
+        flops = 2.0 * dim * nq * float(n - sample_rows)  # the filtered scan over rows [S, n)
+
+        def cpu_sample():
+            import oracle
+            rows = min(n, 262144)
+            Xh = oracle.decode_fp16(X[:rows].cpu().view(torch.int16).numpy())
+            Qh = oracle.decode_fp16(Q[:1].cpu().view(torch.int16).numpy())
+            t0 = time.perf_counter()
+            S = oracle.dense_scores(Qh, Xh)
+            oracle.rank_topk(S, k)
+            dt = time.perf_counter() - t0
+            return 1.0 / (dt * n / rows), (f"1 query against the first {rows} rows, scores + "
+                                           f"top-{k}, extrapolated to all {n} rows")
+
+        cfg = {"workload": "dense_retrieval", "nq": nq, "n": n, "dim": dim, "k": k,
+               "planted": int(w["planted_q"].numel()), "cosine": w["cosine"]}
+        return dict(step=step, pairs=nq, kernel="dense_scan", flops=flops,
+                    metric="top-k queries/sec + % fp16 MFMA peak",
+                    cpu_sample=cpu_sample, config=cfg, dtype="fp16", unit="queries/s",
+                    sha=source_sha("dense.hip", "common.h"), graph=False)
+
     raise SystemExit(f"workload {name} is not available in this build")
 
 
@@ -176,7 +210,7 @@ def main():
     torch.cuda.synchronize()
 
     hpr.kernel_timing(True)
-    for name in ("partition", "maxsim", "maxsim_argmax", "topk", "infonce", "grad_q", "grad_d"):
+    for name in KERNELS:
         hpr.kernel_timing_read(name)  # drop warm-up records (timing was off; no-op)
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
@@ -190,7 +224,7 @@ def main():
     ms = start.elapsed_time(stop) / args.steps
 
     graph_ms = None
-    if not args.no_graph:
+    if not args.no_graph and W.get("graph", True):
         # the same step captured once in a HIP graph and replayed (launch overhead removed)
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())
@@ -211,7 +245,7 @@ def main():
         graph_ms = start.elapsed_time(stop) / args.steps
 
     kernels = {}
-    for name in ("partition", "maxsim", "maxsim_argmax", "topk", "infonce", "grad_q", "grad_d"):
+    for name in KERNELS:
         tot, n = hpr.kernel_timing_read(name)
         if n:
             kernels[name] = {"avg_us": round(1e3 * tot / n, 3), "launches": n}
@@ -232,7 +266,7 @@ def main():
                "sample": sample}
 
     line = {
-        "metric": "MaxSim query x doc pairs/sec + % bf16 MFMA peak",
+        "metric": W.get("metric", "MaxSim query x doc pairs/sec + % bf16 MFMA peak"),
         "value": W["pairs"] / (ms * 1e-3),
         "unit": W["unit"],
         "n_gpus": 1,

@@ -56,6 +56,7 @@ typedef int32_t hpr_status;
 #define HPR_ERR_EMPTY_DOC 3           /* hpr_csr_validate: a document with no token            */
 #define HPR_ERR_UNSUPPORTED_SHAPE 4   /* valid, but outside the limits this build supports     */
 #define HPR_ERR_WORKSPACE_TOO_SMALL 5 /* ws_bytes below the *_workspace_size() value            */
+#define HPR_ERR_CAPACITY 6            /* dense_ip_topk: candidate lists kept overflowing (see it) */
 #define HPR_ERR_HIP 7                 /* a HIP runtime call or kernel launch failed             */
 
 #define HPR_ABI_VERSION 1
@@ -67,7 +68,7 @@ typedef int32_t hpr_status;
  *   Top-k: 1 <= k <= min(n, 1024) (k outside that range is HPR_ERR_INVALID_ARG).
  *   coltrast_loss_fwd_bwd: nq * lq <= 16384 and every document has at most 65536 tokens (the
  *     latter is checked on the device: a longer document makes *loss NaN).
- *   dense_ip_topk: dim % 8 == 0, 8 <= dim <= 8192.
+ *   dense_ip_topk: dim % 8 == 0, 8 <= dim <= 8192; n < 2^31.
  */
 
 /* ---------------------------------------------------------------------------------------------

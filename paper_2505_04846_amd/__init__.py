@@ -30,6 +30,7 @@ STATUS_NAMES = {
     3: "HPR_ERR_EMPTY_DOC",
     4: "HPR_ERR_UNSUPPORTED_SHAPE",
     5: "HPR_ERR_WORKSPACE_TOO_SMALL",
+    6: "HPR_ERR_CAPACITY",
     7: "HPR_ERR_HIP",
 }
 

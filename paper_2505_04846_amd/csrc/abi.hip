@@ -268,16 +268,109 @@ hpr_status coltrast_loss_fwd_bwd(const uint16_t* q, int32_t nq, int32_t lq,
 }
 
 size_t dense_ip_topk_workspace_size(int32_t nq, int64_t n, int32_t dim, int32_t k) {
-  (void)nq, (void)n, (void)dim, (void)k;
-  return 0;
+  if (nq < 1 || n < 1 || dim < 1 || k < 1) return 0;
+  const DensePlan p = dense_plan(n, k);
+  size_t b = align_up((size_t)nq * (size_t)p.S * sizeof(float));  // sample scores
+  if (p.S == n) return b;
+  b += align_up((size_t)nq * k * sizeof(float)) + align_up((size_t)nq * k * sizeof(int64_t));
+  b += align_up((size_t)nq * sizeof(float)) + align_up((size_t)nq * sizeof(int64_t)) +
+       align_up((size_t)nq * sizeof(int32_t));
+  b += align_up((size_t)nq * (size_t)p.cap * sizeof(float)) +
+       align_up((size_t)nq * (size_t)p.cap * sizeof(uint32_t));
+  b += 2 * align_up(sizeof(int32_t)) + 2 * align_up((size_t)nq * sizeof(int32_t));
+  b += align_up((size_t)nq * (size_t)dim * sizeof(uint16_t));
+  return b;
 }
 
 hpr_status dense_ip_topk(const uint16_t* q, int32_t nq, const uint16_t* x, int64_t n,
                          int32_t dim, int32_t k, float* out_scores, int64_t* out_idx, void* ws,
                          size_t ws_bytes, void* stream) {
-  (void)q, (void)nq, (void)x, (void)n, (void)dim, (void)k, (void)out_scores, (void)out_idx;
-  (void)ws, (void)ws_bytes, (void)stream;
-  return fail(HPR_ERR_UNSUPPORTED_SHAPE, "dense_ip_topk is not built yet");
+  if (!q || !x || !out_scores || !out_idx || !ws)
+    return fail(HPR_ERR_INVALID_ARG, "q, x, out_scores, out_idx and ws must be non-NULL");
+  if (nq < 1 || n < 1) return fail(HPR_ERR_INVALID_ARG, "nq (%d) and n (%lld) must be >= 1", nq,
+                                   (long long)n);
+  if (dim < 1) return fail(HPR_ERR_INVALID_ARG, "dim (%d) must be >= 1", dim);
+  if (dim % 8 != 0 || dim < 8 || dim > 8192)
+    return fail(HPR_ERR_UNSUPPORTED_SHAPE, "dense_ip_topk needs dim %% 8 == 0 and 8 <= dim <= 8192 (dim=%d)", dim);
+  if (n >= (int64_t(1) << 31))
+    return fail(HPR_ERR_UNSUPPORTED_SHAPE, "n must be below 2^31 (got %lld)", (long long)n);
+  if (k < 1 || k > 1024 || (int64_t)k > n)
+    return fail(HPR_ERR_INVALID_ARG, "k=%d must satisfy 1 <= k <= min(n, 1024)", k);
+  if (!aligned16(q) || !aligned16(x) || !aligned16(out_scores) || !aligned16(out_idx))
+    return fail(HPR_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+  const size_t need = dense_ip_topk_workspace_size(nq, n, dim, k);
+  if (ws_bytes < need)
+    return fail(HPR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu < %zu bytes", ws_bytes, need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const DensePlan p = dense_plan(n, k);
+  Carver c(ws);
+  float* sample = c.take<float>((size_t)nq * (size_t)p.S * sizeof(float));
+  hipError_t e = timed("dense_sample", s, [&] {
+    return launch_dense_gemm(false, q, nq, nullptr, x, 0, p.S, dim, sample, p.S, nullptr, nullptr,
+                             nullptr, nullptr, nullptr, 0, s);
+  });
+  if (e != hipSuccess) return hip_fail(e, "dense sample launch");
+  if (p.S == n) {  // the sample is the whole store
+    e = timed("topk", s, [&] {
+      return launch_topk_rows(sample, nq, n, n, k, out_scores, out_idx, s);
+    });
+    return e == hipSuccess ? HPR_OK : hip_fail(e, "top-k launch");
+  }
+  float* ss = c.take<float>((size_t)nq * k * sizeof(float));
+  int64_t* si = c.take<int64_t>((size_t)nq * k * sizeof(int64_t));
+  float* theta = c.take<float>((size_t)nq * sizeof(float));
+  int64_t* tie = c.take<int64_t>((size_t)nq * sizeof(int64_t));
+  int32_t* count = c.take<int32_t>((size_t)nq * sizeof(int32_t));
+  float* cand_s = c.take<float>((size_t)nq * (size_t)p.cap * sizeof(float));
+  uint32_t* cand_i = c.take<uint32_t>((size_t)nq * (size_t)p.cap * sizeof(uint32_t));
+  int32_t* ctrl[2];
+  int32_t* qlist[2];
+  ctrl[0] = c.take<int32_t>(sizeof(int32_t));
+  ctrl[1] = c.take<int32_t>(sizeof(int32_t));
+  qlist[0] = c.take<int32_t>((size_t)nq * sizeof(int32_t));
+  qlist[1] = c.take<int32_t>((size_t)nq * sizeof(int32_t));
+  uint16_t* qc = c.take<uint16_t>((size_t)nq * dim * sizeof(uint16_t));
+
+  e = timed("topk", s, [&] { return launch_topk_rows(sample, nq, p.S, p.S, k, ss, si, s); });
+  if (e != hipSuccess) return hip_fail(e, "top-k launch");
+  e = launch_dense_init(ss, nq, k, theta, tie, count, s);
+  if (e != hipSuccess) return hip_fail(e, "dense init launch");
+  e = timed("dense_scan", s, [&] {
+    return launch_dense_gemm(true, q, nq, nullptr, x, p.S, n, dim, nullptr, 0, theta, tie, count,
+                             cand_s, cand_i, p.cap, s);
+  });
+  if (e != hipSuccess) return hip_fail(e, "dense scan launch");
+  e = timed("dense_merge", s, [&] {
+    return launch_dense_merge(ss, si, nq, k, count, cand_s, cand_i, p.cap, nullptr, out_scores, out_idx, theta, tie, ctrl[0], qlist[0], s);
+  });
+  if (e != hipSuccess) return hip_fail(e, "dense merge launch");
+  // Overflowed candidate lists (none unless the sample bound is far from the k-th score) are
+  // rescanned with their raised bounds until every list fits.
+  int cur = 0;
+  for (int round = 0;; ++round) {
+    int32_t m = 0;
+    e = hipMemcpyAsync(&m, ctrl[cur], sizeof(m), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "dense overflow check");
+    if (m == 0) return HPR_OK;
+    if (round == kDenseMaxRepairs)
+      return fail(HPR_ERR_CAPACITY, "candidate lists of %d queries still overflow after %d rescans",
+                  m, kDenseMaxRepairs);
+    const int nxt = cur ^ 1;
+    e = launch_dense_repair_prep(q, dim, qlist[cur], m, qc, count, s);
+    if (e == hipSuccess)
+      e = timed("dense_scan", s, [&] {
+        return launch_dense_gemm(true, qc, m, qlist[cur], x, p.S, n, dim, nullptr, 0, theta, tie,
+                                 count, cand_s, cand_i, p.cap, s);
+      });
+    if (e == hipSuccess)
+      e = timed("dense_merge", s, [&] {
+        return launch_dense_merge(ss, si, m, k, count, cand_s, cand_i, p.cap, qlist[cur], out_scores,
+                                  out_idx, theta, tie, ctrl[nxt], qlist[nxt], s);
+      });
+    if (e != hipSuccess) return hip_fail(e, "dense repair launch");
+    cur = nxt;
+  }
 }
 
 hpr_status hpr_csr_validate(const int64_t* d_off, int64_t n_docs, int64_t n_tok, void* ws,
@@ -350,6 +443,7 @@ const char* hpr_status_string(hpr_status s) {
     case HPR_ERR_EMPTY_DOC: return "HPR_ERR_EMPTY_DOC";
     case HPR_ERR_UNSUPPORTED_SHAPE: return "HPR_ERR_UNSUPPORTED_SHAPE";
     case HPR_ERR_WORKSPACE_TOO_SMALL: return "HPR_ERR_WORKSPACE_TOO_SMALL";
+    case HPR_ERR_CAPACITY: return "HPR_ERR_CAPACITY";
     case HPR_ERR_HIP: return "HPR_ERR_HIP";
     default: return "HPR_ERR_UNKNOWN";
   }

@@ -1,0 +1,444 @@
+// Exact inner-product top-k over a dense fp16 store (pooled single-vector retrieval).
+//
+// s[q, r] = <Q[q], X[r]> (fp16 MFMA, fp32 accumulate); the k best rows per query under
+// (score desc, row asc).  The score matrix is never materialised:
+//
+//   1. Sample.  Rows [0, S) are scored exactly into a workspace matrix and the row top-k of it
+//      is taken (the radix select of topk.hip).  Its k-th score theta_q is a lower bound on the
+//      final k-th score, and every sample row outside the sample top-k is beaten by k sample
+//      rows, so it cannot be in the answer.
+//   2. Scan.  Rows [S, n) are scored by the GEMM kernel below, whose epilogue appends a row to
+//      its query's candidate list only when its key beats the query's bound.  With a random
+//      sample the expected list length is about k (n - S) / S.
+//   3. Merge.  Per query, the exact top-k of (sample top-k) U (candidates) under a unique
+//      64-bit key (score key, ~row).  A list that overflowed its capacity is repaired: its
+//      bound is raised to the k-th key found so far (still a valid bound: k rows reach it) and
+//      rows [S, n) are rescanned for those queries only, until no list overflows.
+//
+// GEMM tile: 256 queries x 256 rows per 8-wave workgroup (each wave 64 x 128 = 2 x 4 blocks of
+// v_mfma_f32_32x32x16_f16); K advances 32 halves per stage through a 4-deep LDS ring filled by
+// direct-to-LDS loads (global_load_lds_dwordx4), so three stages of loads are in flight while
+// one is multiplied.  LDS rows are 64 bytes with the 16-byte chunk c of row r stored at
+// position c ^ ((r >> 2) & 3), which keeps the MFMA operand reads free of bank conflicts.
+// Workgroups that share a row tile are placed on one XCD so its rows come from HBM once.
+#include "common.h"
+#include "kernels.h"
+
+namespace hpr {
+
+namespace {
+
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
+
+constexpr int kTQ = 256;       // queries per workgroup tile
+constexpr int kTR = 256;       // rows per workgroup tile
+constexpr int kKC = 32;        // halves of K per stage
+constexpr int kStages = 4;     // LDS ring depth
+constexpr int kGemmWaves = 8;  // 4 along queries x 2 along rows
+constexpr int kGemmThreads = 64 * kGemmWaves;
+constexpr int kRowBytes = kKC * 2;                      // 64
+constexpr int kTileBytes = kTQ * kRowBytes;             // 16 KiB per operand per stage
+constexpr int kStageBytes = 2 * kTileBytes;             // Q tile then X tile
+constexpr int kLoadsPerWave = kStageBytes / 1024 / kGemmWaves;  // 16-byte loads per lane
+
+// 16 zero bytes in global memory: the source of the K-tail chunks past `dim`.
+__device__ __attribute__((aligned(16))) const uint32_t kZero16[4] = {0u, 0u, 0u, 0u};
+
+struct GemmArgs {
+  const uint16_t* q;      // fp16 [nqa, dim]
+  const uint16_t* x;      // fp16 [n, dim]
+  const int32_t* qmap;    // local query -> global query (nullptr: identity)
+  int nqa;                // queries of this launch
+  int dim;
+  int64_t r0, r1;         // rows [r0, r1) of X
+  int n_qt, n_rt;         // tiles along queries / rows
+  // store mode
+  float* scores;          // [nqa, ld], column c = row r0 + c
+  int64_t ld;
+  // filter mode
+  const float* theta;     // [nq] bound score per global query
+  const int64_t* tie;     // [nq] rows <= tie[q] pass on an equal score (-1: none)
+  int32_t* count;         // [nq] appended candidates
+  float* cand_s;          // [nq, cap]
+  uint32_t* cand_i;       // [nq, cap]
+  int64_t cap;
+};
+
+template <bool FILTER>
+__global__ __launch_bounds__(kGemmThreads, 1) void dense_gemm_kernel(GemmArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wq = wave & 3;   // 64-query slice of the tile
+  const int wr = wave >> 2;  // 128-row slice of the tile
+
+  const int64_t total = (int64_t)a.n_qt * a.n_rt;
+  const int64_t lin = xcd_linear(blockIdx.x, total);
+  const int rt = (int)(lin / a.n_qt);
+  const int qt = (int)(lin - (int64_t)rt * a.n_qt);
+  const int q_base = qt * kTQ;
+  const int64_t row_base = a.r0 + (int64_t)rt * kTR;
+
+  // ---- this lane's direct-to-LDS sources: load j of the wave fills slot g = (4 w + j) 64 + l
+  // of the stage (slots 0..1023: the query tile, 1024..2047: the row tile).
+  const char* src[kLoadsPerWave];
+  int src_c[kLoadsPerWave];
+#pragma unroll
+  for (int j = 0; j < kLoadsPerWave; ++j) {
+    const int g = (wave * kLoadsPerWave + j) * 64 + lane;
+    const bool is_x = g >= 1024;
+    const int local = g & 1023;
+    const int r = local >> 2;
+    const int c = (local & 3) ^ ((r >> 2) & 3);
+    int64_t row;
+    const uint16_t* base;
+    if (is_x) {
+      row = row_base + r;
+      row = row < a.r1 ? row : a.r1 - 1;
+      base = a.x;
+    } else {
+      int qq = q_base + r;
+      qq = qq < a.nqa ? qq : a.nqa - 1;
+      row = qq;
+      base = a.q;
+    }
+    src[j] = reinterpret_cast<const char*>(base + row * a.dim + 8 * c);
+    src_c[j] = 8 * c;
+  }
+  auto issue_stage = [&](int kk) {
+    unsigned char* st = smem + (kk % kStages) * kStageBytes;
+    const int k0 = kk * kKC;
+#pragma unroll
+    for (int j = 0; j < kLoadsPerWave; ++j) {
+      const void* p = (k0 + src_c[j] < a.dim) ? (const void*)(src[j] + 2 * (int64_t)k0)
+                                               : (const void*)kZero16;
+      __builtin_amdgcn_global_load_lds((glb_void_t*)p,
+                                       (lds_void_t*)(st + (wave * kLoadsPerWave + j) * 1024), 16,
+                                       0, 0);
+    }
+  };
+
+  // ---- per-lane LDS offsets of the MFMA operands: row `col` of block b, chunk 2 s + half
+  const int col = lane & 31, half = lane >> 5;
+  uint32_t offq[2][2], offx[4][2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int c = 2 * s + half;
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int r = wq * 64 + 32 * b + col;
+      offq[b][s] = r * kRowBytes + 16 * (c ^ ((r >> 2) & 3));
+    }
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int r = wr * 128 + 32 * b + col;
+      offx[b][s] = kTileBytes + r * kRowBytes + 16 * (c ^ ((r >> 2) & 3));
+    }
+  }
+
+  f32x16 acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int nk = (a.dim + kKC - 1) / kKC;
+#pragma unroll
+  for (int s = 0; s < kStages - 1; ++s)
+    if (s < nk) issue_stage(s);
+
+#pragma unroll 1
+  for (int kk = 0; kk < nk; ++kk) {
+    // this wave's loads of stage kk have landed once at most the later stages' are pending
+    const int later = (nk - 1 - kk) < (kStages - 2) ? (nk - 1 - kk) : (kStages - 2);
+    if (later >= 2)
+      __builtin_amdgcn_s_waitcnt(0x0f70 | (2 * kLoadsPerWave));
+    else if (later == 1)
+      __builtin_amdgcn_s_waitcnt(0x0f70 | kLoadsPerWave);
+    else
+      __builtin_amdgcn_s_waitcnt(0x0f70);
+    // every wave's operand reads of stage kk - 1 are complete (lgkmcnt(0)) before the barrier,
+    // so the buffer they used can be refilled right after it
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    if (kk + kStages - 1 < nk) issue_stage(kk + kStages - 1);
+
+    const unsigned char* st = smem + (kk % kStages) * kStageBytes;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      f16x8 fa[2], fb[4];
+#pragma unroll
+      for (int b = 0; b < 2; ++b) fa[b] = as_f16x8(*reinterpret_cast<const u32x4*>(st + offq[b][s]));
+#pragma unroll
+      for (int b = 0; b < 4; ++b) fb[b] = as_f16x8(*reinterpret_cast<const u32x4*>(st + offx[b][s]));
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+  }
+
+  // ---- epilogue.  acc[i][j] register r: query q_base + 64 wq + 32 i + 8 (r / 4) + 4 half
+  // + r % 4, row row_base + 128 wr + 32 j + col.
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int ql = q_base + 64 * wq + 32 * i + 8 * (r >> 2) + 4 * half + (r & 3);
+      if (ql >= a.nqa) continue;
+      if (!FILTER) {
+        float* dst = a.scores + (int64_t)ql * a.ld + (row_base - a.r0) + 128 * wr + col;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int64_t row = row_base + 128 * wr + 32 * j + col;
+          if (row < a.r1) dst[32 * j] = acc[i][j][r];
+        }
+      } else {
+        const int gq = a.qmap ? a.qmap[ql] : ql;
+        const float th = a.theta[gq];
+        const int64_t tie = a.tie[gq];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int64_t row = row_base + 128 * wr + 32 * j + col;
+          const float v = acc[i][j][r];
+          if (row < a.r1 && (v > th || (v == th && row <= tie))) {
+            const int p = atomicAdd(&a.count[gq], 1);
+            if (p < a.cap) {
+              a.cand_s[(int64_t)gq * a.cap + p] = v;
+              a.cand_i[(int64_t)gq * a.cap + p] = (uint32_t)row;
+            }
+          }
+        }
+      }
+    }
+  }
+}
+
+// Bound of every query from its sample top-k: theta = k-th score, strict comparison; lists
+// emptied.
+__global__ void dense_init_kernel(const float* ss, int nq, int k, float* theta, int64_t* tie,
+                                  int32_t* count) {
+  const int q = blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= nq) return;
+  theta[q] = ss[(int64_t)q * k + k - 1];
+  tie[q] = -1;
+  count[q] = 0;
+}
+
+// Queries to rescan: their Q rows are gathered (qc) and their lists emptied.
+__global__ void dense_repair_prep_kernel(const uint16_t* q, int dim, const int32_t* qlist,
+                                         int m, uint16_t* qc, int32_t* count) {
+  for (int i = blockIdx.x; i < m; i += gridDim.x) {
+    const int gq = qlist[i];
+    const u32x4* s = reinterpret_cast<const u32x4*>(q + (int64_t)gq * dim);
+    u32x4* d = reinterpret_cast<u32x4*>(qc + (int64_t)i * dim);
+    for (int c = threadIdx.x; c < dim / 8; c += blockDim.x) d[c] = s[c];
+    if (threadIdx.x == 0) count[gq] = 0;
+  }
+}
+
+constexpr int kMergeThreads = 1024;
+constexpr int kMergeMaxK = 1024;
+
+// Exact top-k of (sample top-k of query q) U (its candidates) under the unique key
+// (score key << 32) | ~row: 8 radix passes of 8 bits find the k-th key K, the elements with key
+// >= K are gathered (exactly k: keys are unique) and bitonic-sorted.  A query whose list
+// overflowed gets its bound raised to K and is queued for a rescan (*ctrl_out counts them,
+// qlist_out lists them); its output is rewritten after the rescan.
+__global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(
+    const float* ss, const int64_t* si, int k, const int32_t* count, const float* cand_s,
+    const uint32_t* cand_i, int64_t cap, const int32_t* qsel, float* out_s, int64_t* out_i,
+    float* theta, int64_t* tie, int32_t* ctrl_out, int32_t* qlist_out) {
+  __shared__ uint32_t hist[256];
+  __shared__ unsigned long long sk[kMergeMaxK];
+  __shared__ uint32_t sh_bin, sh_above, sh_n;
+  const int q = qsel ? qsel[blockIdx.x] : (int)blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int cnt = count[q];
+  const int64_t m_c = cnt < cap ? cnt : cap;
+  const int64_t m = k + m_c;
+  auto key_at = [&](int64_t e) -> unsigned long long {
+    float s;
+    uint32_t row;
+    if (e < k) {
+      s = ss[(int64_t)q * k + e];
+      row = (uint32_t)si[(int64_t)q * k + e];
+    } else {
+      s = cand_s[(int64_t)q * cap + (e - k)];
+      row = cand_i[(int64_t)q * cap + (e - k)];
+    }
+    return ((unsigned long long)score_key(s) << 32) | (unsigned long long)(~row);
+  };
+
+  unsigned long long prefix = 0, pmask = 0;
+  uint32_t remaining = (uint32_t)k;
+  for (int pass = 0; pass < 8; ++pass) {
+    const int shift = 56 - 8 * pass;
+    if (tid < 256) hist[tid] = 0;
+    if (tid == 0) {
+      sh_bin = 0;
+      sh_above = 0;
+    }
+    __syncthreads();
+    for (int64_t e = tid; e < m; e += kMergeThreads) {
+      const unsigned long long key = key_at(e);
+      if ((key & pmask) == prefix) atomicAdd(&hist[(uint32_t)(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (wave == 0) {
+      uint32_t c[4], tot = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        c[j] = hist[255 - 4 * lane - j];
+        tot += c[j];
+      }
+      uint32_t incl = tot;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(incl, o);
+        if (lane >= o) incl += y;
+      }
+      const uint32_t excl = incl - tot;
+      if (excl < remaining && remaining <= incl) {
+        uint32_t accu = excl;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (accu + c[j] >= remaining) {
+            sh_bin = 255u - 4u * lane - j;
+            sh_above = accu;
+            break;
+          }
+          accu += c[j];
+        }
+      }
+    }
+    __syncthreads();
+    prefix |= (unsigned long long)sh_bin << shift;
+    pmask |= 255ull << shift;
+    remaining -= sh_above;
+    __syncthreads();
+  }
+  const unsigned long long K = prefix;  // the k-th largest key
+
+  if (tid == 0) sh_n = 0;
+  __syncthreads();
+  for (int64_t e = tid; e < m; e += kMergeThreads) {
+    const unsigned long long key = key_at(e);
+    if (key >= K) {
+      const uint32_t p = atomicAdd(&sh_n, 1u);
+      if (p < (uint32_t)k) sk[p] = key;
+    }
+  }
+  __syncthreads();
+  uint32_t P = 1;
+  while (P < (uint32_t)k) P <<= 1;
+  for (uint32_t i = k + tid; i < P; i += kMergeThreads) sk[i] = 0ull;
+  for (uint32_t size = 2; size <= P; size <<= 1) {
+    for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
+      __syncthreads();
+      for (uint32_t i = tid; i < P; i += kMergeThreads) {
+        const uint32_t j = i ^ stride;
+        if (j > i) {
+          const bool up = (i & size) == 0;  // descending runs where `up`
+          const unsigned long long ki = sk[i], kj = sk[j];
+          if ((kj > ki) == up) {
+            sk[i] = kj;
+            sk[j] = ki;
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+  for (int p = tid; p < k; p += kMergeThreads) {
+    out_s[(int64_t)q * k + p] = key_score((uint32_t)(sk[p] >> 32));
+    out_i[(int64_t)q * k + p] = (int64_t)(uint32_t)~(uint32_t)sk[p];
+  }
+  if (cnt > cap && tid == 0) {
+    theta[q] = key_score((uint32_t)(K >> 32));
+    tie[q] = (int64_t)(uint32_t)~(uint32_t)K;
+    const int slot = atomicAdd(&ctrl_out[0], 1);
+    qlist_out[slot] = q;
+  }
+}
+
+__global__ void dense_zero_ctrl_kernel(int32_t* ctrl) { ctrl[0] = 0; }
+
+}  // namespace
+
+hipError_t launch_dense_gemm(bool filter, const uint16_t* q, int nqa, const int32_t* qmap,
+                             const uint16_t* x, int64_t r0, int64_t r1, int dim, float* scores,
+                             int64_t ld, const float* theta, const int64_t* tie, int32_t* count,
+                             float* cand_s, uint32_t* cand_i, int64_t cap, hipStream_t stream) {
+  GemmArgs a;
+  a.q = q;
+  a.x = x;
+  a.qmap = qmap;
+  a.nqa = nqa;
+  a.dim = dim;
+  a.r0 = r0;
+  a.r1 = r1;
+  a.n_qt = (nqa + kTQ - 1) / kTQ;
+  const int64_t n_rt = (r1 - r0 + kTR - 1) / kTR;
+  if (nqa < 1 || n_rt < 1 || n_rt > 0x7fffffffLL || (int64_t)a.n_qt * n_rt > 0xffffffffLL)
+    return hipErrorInvalidValue;
+  a.n_rt = (int)n_rt;
+  a.scores = scores;
+  a.ld = ld;
+  a.theta = theta;
+  a.tie = tie;
+  a.count = count;
+  a.cand_s = cand_s;
+  a.cand_i = cand_i;
+  a.cap = cap;
+  const int lds = kStages * kStageBytes;
+  const unsigned blocks = (unsigned)((int64_t)a.n_qt * n_rt);
+  const void* fn = filter ? (const void*)dense_gemm_kernel<true> : (const void*)dense_gemm_kernel<false>;
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) return e;
+  if (filter)
+    hipLaunchKernelGGL(dense_gemm_kernel<true>, dim3(blocks), dim3(kGemmThreads), lds, stream, a);
+  else
+    hipLaunchKernelGGL(dense_gemm_kernel<false>, dim3(blocks), dim3(kGemmThreads), lds, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_dense_init(const float* ss, int nq, int k, float* theta, int64_t* tie,
+                             int32_t* count, hipStream_t stream) {
+  hipLaunchKernelGGL(dense_init_kernel, dim3((nq + 255) / 256), dim3(256), 0, stream, ss, nq, k,
+                     theta, tie, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_dense_merge(const float* ss, const int64_t* si, int nq_grid, int k,
+                              const int32_t* count, const float* cand_s, const uint32_t* cand_i,
+                              int64_t cap, const int32_t* qsel, float* out_s, int64_t* out_i,
+                              float* theta, int64_t* tie, int32_t* ctrl_out, int32_t* qlist_out,
+                              hipStream_t stream) {
+  if (k < 1 || k > kMergeMaxK || nq_grid < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(dense_zero_ctrl_kernel, dim3(1), dim3(1), 0, stream, ctrl_out);
+  hipLaunchKernelGGL(dense_merge_kernel, dim3((unsigned)nq_grid), dim3(kMergeThreads), 0, stream,
+                     ss, si, k, count, cand_s, cand_i, cap, qsel, out_s, out_i, theta, tie,
+                     ctrl_out, qlist_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_dense_repair_prep(const uint16_t* q, int dim, const int32_t* qlist, int m,
+                                    uint16_t* qc, int32_t* count, hipStream_t stream) {
+  if (m < 1) return hipSuccess;
+  const int blocks = m < 1024 ? m : 1024;
+  hipLaunchKernelGGL(dense_repair_prep_kernel, dim3(blocks), dim3(256), 0, stream, q, dim, qlist,
+                     m, qc, count);
+  return hipGetLastError();
+}
+
+}  // namespace hpr

@@ -68,4 +68,47 @@ hipError_t launch_grad_d(const uint16_t* q, const int64_t* off, int64_t n_docs, 
 
 hipError_t launch_scale(float* x, int64_t n, const float* scale, hipStream_t stream);
 
+// Dense inner-product top-k ----------------------------------------------------------------------
+// Rows [0, S) are the exact sample; candidate lists hold `cap` entries per query.
+struct DensePlan {
+  int64_t S;
+  int64_t cap;
+};
+inline DensePlan dense_plan(int64_t n, int k) {
+  DensePlan p;
+  const int64_t target = (int64_t)32 * k > 131072 ? (int64_t)32 * k : 131072;
+  p.S = n < target ? n : target;
+  if (p.S == n) {
+    p.cap = 0;
+  } else {
+    const int64_t expect = ((int64_t)k * (n - p.S) + p.S - 1) / p.S;
+    int64_t cap = 4 * expect + 256;
+    cap = cap > 1024 ? cap : 1024;
+    p.cap = (cap + 63) / 64 * 64;
+  }
+  return p;
+}
+constexpr int kDenseMaxRepairs = 16;
+
+// Scores of queries q[0 .. nqa) (fp16 [nqa, dim]) against rows [r0, r1) of x.  Store mode
+// (filter = false) writes them to scores[q * ld + (r - r0)]; filter mode appends (score, row)
+// to the list of global query g = qmap ? qmap[q] : q when the score beats (theta[g], tie[g]).
+hipError_t launch_dense_gemm(bool filter, const uint16_t* q, int nqa, const int32_t* qmap,
+                             const uint16_t* x, int64_t r0, int64_t r1, int dim, float* scores,
+                             int64_t ld, const float* theta, const int64_t* tie, int32_t* count,
+                             float* cand_s, uint32_t* cand_i, int64_t cap, hipStream_t stream);
+// theta[q] = ss[q, k-1], tie[q] = -1, count[q] = 0.
+hipError_t launch_dense_init(const float* ss, int nq, int k, float* theta, int64_t* tie,
+                             int32_t* count, hipStream_t stream);
+// Final top-k of (sample top-k) U (candidates) for queries qsel[0 .. nq_grid) (or 0 .. nq_grid
+// when qsel is null); *ctrl_out / qlist_out receive the queries whose lists overflowed.
+hipError_t launch_dense_merge(const float* ss, const int64_t* si, int nq_grid, int k,
+                              const int32_t* count, const float* cand_s, const uint32_t* cand_i,
+                              int64_t cap, const int32_t* qsel, float* out_s, int64_t* out_i,
+                              float* theta, int64_t* tie, int32_t* ctrl_out, int32_t* qlist_out,
+                              hipStream_t stream);
+// Gathers the m queued queries' rows into qc and empties their lists.
+hipError_t launch_dense_repair_prep(const uint16_t* q, int dim, const int32_t* qlist, int m,
+                                    uint16_t* qc, int32_t* count, hipStream_t stream);
+
 }  // namespace hpr
