@@ -173,8 +173,11 @@ size_t coltrast_loss_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int6
   if (nq < 1 || lq < 1 || n_docs < 1) return 0;
   const size_t sd = align_up((size_t)nq * (size_t)n_docs * sizeof(float));
   const size_t am = align_up((size_t)n_docs * (size_t)nq * (size_t)lq * sizeof(uint16_t));
+  const int64_t E = (int64_t)nq * lq;
+  const size_t gq = align_up((size_t)grad_q_ranges(n_docs, n_tok, E, dim) * (size_t)E *
+                             (size_t)dim * sizeof(float));
   return 2 * sd + am + part_bytes(n_docs) + align_up(2 * sizeof(int32_t)) +
-         align_up((size_t)nq * sizeof(float));
+         align_up((size_t)nq * sizeof(float)) + gq;
 }
 
 hpr_status maxsim_score(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d_tok,
@@ -246,6 +249,8 @@ hpr_status coltrast_loss_fwd_bwd(const uint16_t* q, int32_t nq, int32_t lq,
   int64_t* part = c.take<int64_t>(part_bytes(n_docs));
   int32_t* ctrl = c.take<int32_t>(2 * sizeof(int32_t));
   float* terms = c.take<float>((size_t)nq * sizeof(float));
+  float* gq_part = c.take<float>((size_t)grad_q_ranges(n_docs, n_tok, (int64_t)nq * lq, dim) *
+                                 (size_t)nq * lq * dim * sizeof(float));
   st = run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, S, amax, ctrl, part, s);
   if (st != HPR_OK) return st;
   hipError_t e = timed("infonce", s, [&] {
@@ -254,7 +259,7 @@ hpr_status coltrast_loss_fwd_bwd(const uint16_t* q, int32_t nq, int32_t lq,
   if (e != hipSuccess) return hip_fail(e, "infonce launch");
   if (dq) {
     e = timed("grad_q", s, [&] {
-      return launch_grad_q(d_tok, d_off, n_docs, n_tok, dim, nq, lq, amax, G, dq, s);
+      return launch_grad_q(d_tok, d_off, n_docs, n_tok, dim, nq, lq, amax, G, gq_part, dq, s);
     });
     if (e != hipSuccess) return hip_fail(e, "dQ launch");
   }

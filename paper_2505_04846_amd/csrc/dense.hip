@@ -17,10 +17,13 @@
 //
 // GEMM tile: 256 queries x 256 rows per 8-wave workgroup (each wave 64 x 128 = 2 x 4 blocks of
 // v_mfma_f32_32x32x16_f16); K advances 32 halves per stage through a 4-deep LDS ring filled by
-// direct-to-LDS loads (global_load_lds_dwordx4), so three stages of loads are in flight while
-// one is multiplied.  LDS rows are 64 bytes with the 16-byte chunk c of row r stored at
-// position c ^ ((r >> 2) & 3), which keeps the MFMA operand reads free of bank conflicts.
-// Workgroups that share a row tile are placed on one XCD so its rows come from HBM once.
+// direct-to-LDS loads (global_load_lds_dwordx4, a wave-uniform base plus 32-bit lane offsets),
+// so two to three stages of loads are in flight while one is multiplied.  The loop is software
+// pipelined with one barrier per stage, placed between the stage's two k-steps: the next
+// stage's first operands are read from LDS while the current stage's last MFMAs run.  LDS rows
+// are 64 bytes with the 16-byte chunk c of row r stored at position c ^ ((r >> 2) & 3), which
+// keeps the MFMA operand reads free of bank conflicts (measured: none).  Workgroups that share
+// a row tile are placed on one XCD so its rows come from HBM about once.
 #include "common.h"
 #include "kernels.h"
 
@@ -83,41 +86,50 @@ __global__ __launch_bounds__(kGemmThreads, 1) void dense_gemm_kernel(GemmArgs a)
   const int64_t row_base = a.r0 + (int64_t)rt * kTR;
 
   // ---- this lane's direct-to-LDS sources: load j of the wave fills slot g = (4 w + j) 64 + l
-  // of the stage (slots 0..1023: the query tile, 1024..2047: the row tile).
-  const char* src[kLoadsPerWave];
+  // of the stage (slots 0..1023: the query tile, 1024..2047: the row tile).  The source is a
+  // wave-uniform base (the tile's first row, advanced by each stage's K offset) plus a 32-bit
+  // per-lane byte offset (row within the tile, clamped to the last valid row, and chunk).
+  const bool wave_x = wave * kLoadsPerWave * 64 >= 1024;  // uniform: waves 4..7 load the rows
+  const char* tile_base;
+  {
+    const int64_t first = wave_x ? row_base : (int64_t)q_base;
+    tile_base = reinterpret_cast<const char*>((wave_x ? a.x : a.q) + first * a.dim);
+  }
+  const int64_t tile_rows = wave_x ? (a.r1 - row_base) : (int64_t)(a.nqa - q_base);
+  uint32_t voff[kLoadsPerWave];
   int src_c[kLoadsPerWave];
 #pragma unroll
   for (int j = 0; j < kLoadsPerWave; ++j) {
     const int g = (wave * kLoadsPerWave + j) * 64 + lane;
-    const bool is_x = g >= 1024;
     const int local = g & 1023;
-    const int r = local >> 2;
+    int r = local >> 2;
     const int c = (local & 3) ^ ((r >> 2) & 3);
-    int64_t row;
-    const uint16_t* base;
-    if (is_x) {
-      row = row_base + r;
-      row = row < a.r1 ? row : a.r1 - 1;
-      base = a.x;
-    } else {
-      int qq = q_base + r;
-      qq = qq < a.nqa ? qq : a.nqa - 1;
-      row = qq;
-      base = a.q;
-    }
-    src[j] = reinterpret_cast<const char*>(base + row * a.dim + 8 * c);
+    r = r < tile_rows ? r : (int)tile_rows - 1;
+    voff[j] = (uint32_t)r * (uint32_t)a.dim * 2u + 16u * c;
     src_c[j] = 8 * c;
   }
-  auto issue_stage = [&](int kk) {
+  const bool k_tail = (a.dim % kKC) != 0;
+  // Loads stage `src_kk` of K into the ring buffer of stage `kk` (src_kk < kk only for the
+  // filler stages past the last one, which keep the number of stages in flight constant).
+  auto issue_stage = [&](int kk, int src_kk) {
     unsigned char* st = smem + (kk % kStages) * kStageBytes;
-    const int k0 = kk * kKC;
+    const int k0 = src_kk * kKC;
+    const char* base = tile_base + 2 * (int64_t)k0;
+    if (!k_tail || k0 + kKC <= a.dim) {
 #pragma unroll
-    for (int j = 0; j < kLoadsPerWave; ++j) {
-      const void* p = (k0 + src_c[j] < a.dim) ? (const void*)(src[j] + 2 * (int64_t)k0)
-                                               : (const void*)kZero16;
-      __builtin_amdgcn_global_load_lds((glb_void_t*)p,
-                                       (lds_void_t*)(st + (wave * kLoadsPerWave + j) * 1024), 16,
-                                       0, 0);
+      for (int j = 0; j < kLoadsPerWave; ++j)
+        __builtin_amdgcn_global_load_lds((glb_void_t*)(base + voff[j]),
+                                         (lds_void_t*)(st + (wave * kLoadsPerWave + j) * 1024),
+                                         16, 0, 0);
+    } else {  // the last, partial K chunk: chunks past `dim` read 16 zero bytes
+#pragma unroll
+      for (int j = 0; j < kLoadsPerWave; ++j) {
+        const void* p = (k0 + src_c[j] < a.dim) ? (const void*)(base + voff[j])
+                                                 : (const void*)kZero16;
+        __builtin_amdgcn_global_load_lds((glb_void_t*)p,
+                                         (lds_void_t*)(st + (wave * kLoadsPerWave + j) * 1024),
+                                         16, 0, 0);
+      }
     }
   };
 
@@ -147,44 +159,57 @@ __global__ __launch_bounds__(kGemmThreads, 1) void dense_gemm_kernel(GemmArgs a)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  // Software pipeline over the K stages.  Every iteration issues exactly one stage of loads
+  // (past the last stage it reloads the last one into a buffer nobody reads again), so "stage
+  // kk+1 has landed" is always "at most one stage of this wave's loads is still in flight".
   const int nk = (a.dim + kKC - 1) / kKC;
 #pragma unroll
-  for (int s = 0; s < kStages - 1; ++s)
-    if (s < nk) issue_stage(s);
+  for (int s = 0; s < kStages - 1; ++s) issue_stage(s, s < nk ? s : nk - 1);
 
-#pragma unroll 1
-  for (int kk = 0; kk < nk; ++kk) {
-    // this wave's loads of stage kk have landed once at most the later stages' are pending
-    const int later = (nk - 1 - kk) < (kStages - 2) ? (nk - 1 - kk) : (kStages - 2);
-    if (later >= 2)
-      __builtin_amdgcn_s_waitcnt(0x0f70 | (2 * kLoadsPerWave));
-    else if (later == 1)
-      __builtin_amdgcn_s_waitcnt(0x0f70 | kLoadsPerWave);
-    else
-      __builtin_amdgcn_s_waitcnt(0x0f70);
-    // every wave's operand reads of stage kk - 1 are complete (lgkmcnt(0)) before the barrier,
-    // so the buffer they used can be refilled right after it
-    __builtin_amdgcn_s_waitcnt(0xc07f);
+  struct Frags {
+    f16x8 a[2], b[4];
+  };
+  auto read_frags = [&](int kk, int s, Frags& f) {
+    const unsigned char* st = smem + (kk % kStages) * kStageBytes;
+#pragma unroll
+    for (int b = 0; b < 2; ++b) f.a[b] = as_f16x8(*reinterpret_cast<const u32x4*>(st + offq[b][s]));
+#pragma unroll
+    for (int b = 0; b < 4; ++b) f.b[b] = as_f16x8(*reinterpret_cast<const u32x4*>(st + offx[b][s]));
+  };
+  auto mfma = [&](const Frags& f) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+  };
+  auto barrier = [&]() {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     __builtin_amdgcn_s_barrier();
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    if (kk + kStages - 1 < nk) issue_stage(kk + kStages - 1);
+  };
 
-    const unsigned char* st = smem + (kk % kStages) * kStageBytes;
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      f16x8 fa[2], fb[4];
-#pragma unroll
-      for (int b = 0; b < 2; ++b) fa[b] = as_f16x8(*reinterpret_cast<const u32x4*>(st + offq[b][s]));
-#pragma unroll
-      for (int b = 0; b < 4; ++b) fb[b] = as_f16x8(*reinterpret_cast<const u32x4*>(st + offx[b][s]));
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-    }
+  Frags f0, f1;
+  __builtin_amdgcn_s_waitcnt(0x0f70 | (2 * kLoadsPerWave));  // stage 0 landed (this wave)
+  barrier();                                                // ... and for every wave
+  read_frags(0, 0, f0);
+#pragma unroll 1
+  for (int kk = 0; kk < nk; ++kk) {
+    read_frags(kk, 1, f1);
+    mfma(f0);
+    // Stage kk+1 lands everywhere, and every wave's reads of stage kk-1 are complete (this
+    // wave's LDS reads drain before the barrier), so that stage's buffer ((kk + 3) % 4) can
+    // take stage kk+3.
+    __builtin_amdgcn_s_waitcnt(0x0f70 | kLoadsPerWave);
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+    barrier();
+    const int nxt = kk + kStages - 1;
+    issue_stage(nxt, nxt < nk ? nxt : nk - 1);
+    read_frags(kk + 1 < nk ? kk + 1 : kk, 0, f0);
+    __builtin_amdgcn_sched_barrier(0);  // the next stage's reads go out before these MFMAs
+    mfma(f1);
   }
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // no load may still target LDS when the kernel ends
 
   // ---- epilogue.  acc[i][j] register r: query q_base + 64 wq + 32 i + 8 (r / 4) + 4 half
   // + r % 4, row row_base + 128 wr + 32 j + col.

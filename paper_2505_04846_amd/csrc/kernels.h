@@ -58,9 +58,12 @@ hipError_t launch_infonce(const float* S, int nq, int64_t n_docs, const int32_t*
                           float scale, float* G, float* terms, float* loss, float* scores_out,
                           int32_t* ctrl, hipStream_t stream);
 
+// dQ in two passes over `grad_q_ranges` document ranges; part holds
+// grad_q_ranges(...) * nq * lq * dim floats of partial sums.
+int grad_q_ranges(int64_t n_docs, int64_t n_tok, int64_t E, int dim);
 hipError_t launch_grad_q(const uint16_t* d_tok, const int64_t* off, int64_t n_docs, int64_t n_tok,
-                         int dim, int nq, int lq, const uint16_t* amax, const float* G, float* dq,
-                         hipStream_t stream);
+                         int dim, int nq, int lq, const uint16_t* amax, const float* G,
+                         float* part, float* dq, hipStream_t stream);
 
 hipError_t launch_grad_d(const uint16_t* q, const int64_t* off, int64_t n_docs, int64_t n_tok,
                          int dim, int nq, int lq, const uint16_t* amax, const float* G, float* dd,

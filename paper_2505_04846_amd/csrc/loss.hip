@@ -2,12 +2,13 @@
 //
 //   infonce_kernel  one workgroup: per query row the max logit, a log1p-form log-sum-exp, the
 //                   loss term and G = dloss/dS; the batch mean is reduced in a fixed order.
-//   grad_q_kernel   dQ[q,i,:] = sum_d G[q,d] * D[argmax token of (q,i,d)]: one wave per 4 query
-//                   tokens of one query; 16 lanes per token, 8 columns per lane.
+//   grad_q_*        dQ[q,i,:] = sum_d G[q,d] * D[argmax token of (q,i,d)]: partial sums over
+//                   XCD-local document ranges (the gathered rows hit L2), then a fixed-order
+//                   sum over the ranges.
 //   grad_d_kernel   dD: one workgroup per document.  The (q,i) entries are sorted by the token
-//                   they selected (bitonic sort of (token << 14 | entry) keys in LDS), then each
-//                   token row is summed over its entries in entry order, so the result is
-//                   deterministic without atomics; rows nobody selected are written as zeros.
+//                   they selected (stable counting sort in LDS), then each token row is summed
+//                   over its entries in entry order, so the result is deterministic without
+//                   atomics; rows nobody selected are written as zeros.
 #include "common.h"
 #include "kernels.h"
 
@@ -134,33 +135,33 @@ __global__ __launch_bounds__(kRowThreads) void infonce_kernel(const float* __res
   }
 }
 
-constexpr int kGqWaves = 16;
+constexpr int kGqWaves = 4;
+constexpr int kGqThreads = 64 * kGqWaves;
+constexpr int kGqEntries = 4 * kGqWaves;  // (q, i) entries per workgroup: 16 lanes each
 constexpr int kGqUnroll = 8;
 
-// dQ: one workgroup per (query q, group of 4 query tokens); wave w sums a contiguous chunk of
-// the documents, keeping kGqUnroll independent row gathers in flight; the 16 partial sums are
-// then added in wave order (deterministic).  Lane: token (lane >> 4), 8 columns at
-// 8 * ((lane & 15) + 16 cc).
+// dQ, first pass: workgroup (r, g) sums, for the 16 entries e = q * lq + i of group g, the
+// gathered rows G[q,d] * D[token a(q,i,d)] over the documents of range r.  Ranges are placed on
+// XCDs so that a range's document rows are gathered from its L2.  Lane: entry (lane >> 4),
+// 8 columns at 8 * ((lane & 15) + 16 cc).  Partials part[r][e][:] are summed by the second pass
+// in range order, so the result does not depend on scheduling.
 template <int CPL>
-__global__ __launch_bounds__(64 * kGqWaves) void grad_q_kernel(
+__global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
     const uint16_t* __restrict__ D, const int64_t* __restrict__ off, int64_t n_docs,
     int64_t n_tok, int dim, int nq, int lq, const uint16_t* __restrict__ amax,
-    const float* __restrict__ G, float* dq) {
-  __shared__ float part[kGqWaves][4][128 * CPL];
+    const float* __restrict__ G, float* __restrict__ part, int n_groups, int R) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int groups = (lq + 3) / 4;
-  const int q = blockIdx.x / groups;
-  const int i0 = (blockIdx.x - q * groups) * 4;
-  const int sub = lane >> 4;
-  const int i = i0 + sub;
-  const bool active = i < lq;
-  const int c = lane & 15;
+  const int64_t lin = xcd_linear(blockIdx.x, (int64_t)n_groups * R);
+  const int r = (int)(lin / n_groups);
+  const int grp = (int)(lin - (int64_t)r * n_groups);
   const int64_t E = (int64_t)nq * lq;
-  const int64_t e = (int64_t)q * lq + (active ? i : 0);
+  const int64_t e = (int64_t)grp * kGqEntries + wave * 4 + (lane >> 4);
+  const bool active = e < E;
+  const int64_t ee = active ? e : 0;
+  const int64_t q = ee / lq;
+  const int c = lane & 15;
+  const int64_t d0 = n_docs * r / R, d1 = n_docs * (r + 1) / R;
   const int64_t last_tok = n_tok - 1;
-  const int64_t chunk = (n_docs + kGqWaves - 1) / kGqWaves;
-  const int64_t dbeg = wave * chunk;
-  const int64_t dend = dbeg + chunk < n_docs ? dbeg + chunk : n_docs;
 
   float acc[CPL][8];
 #pragma unroll
@@ -168,18 +169,18 @@ __global__ __launch_bounds__(64 * kGqWaves) void grad_q_kernel(
 #pragma unroll
     for (int v = 0; v < 8; ++v) acc[cc][v] = 0.f;
 
-  for (int64_t d0 = dbeg; d0 < dend; d0 += kGqUnroll) {
+  for (int64_t db = d0; db < d1; db += kGqUnroll) {
     float g[kGqUnroll];
     int64_t row[kGqUnroll];
 #pragma unroll
     for (int u = 0; u < kGqUnroll; ++u) {
-      const int64_t d = d0 + u;
-      const bool ok = d < dend;
-      g[u] = ok ? G[(int64_t)q * n_docs + d] : 0.f;
+      const int64_t d = db + u;
+      const bool ok = d < d1;
+      g[u] = ok ? G[q * n_docs + d] : 0.f;
       int64_t base = ok ? off[d] : 0;
       base = base < 0 ? 0 : (base > last_tok ? last_tok : base);
-      const int64_t r = base + (ok ? amax[d * E + e] : 0);
-      row[u] = r > last_tok ? last_tok : r;
+      const int64_t rr = base + (ok ? amax[d * E + ee] : 0);
+      row[u] = rr > last_tok ? last_tok : rr;
     }
     u32x4 w[kGqUnroll][CPL];
 #pragma unroll
@@ -203,140 +204,221 @@ __global__ __launch_bounds__(64 * kGqWaves) void grad_q_kernel(
         acc[cc][7] += g[u] * bf16_hi(w[u][cc].w);
       }
   }
+  if (!active) return;
+  float* dst = part + ((int64_t)r * E + e) * dim;
 #pragma unroll
-  for (int cc = 0; cc < CPL; ++cc)
-#pragma unroll
-    for (int v = 0; v < 8; ++v) part[wave][sub][8 * (c + 16 * cc) + v] = acc[cc][v];
-  __syncthreads();
-  for (int o = tid; o < 4 * 128 * CPL; o += 64 * kGqWaves) {
-    const int t = o / (128 * CPL), k = o % (128 * CPL);
-    if (i0 + t < lq && k < dim) {
-      float v = 0.f;
-#pragma unroll
-      for (int w2 = 0; w2 < kGqWaves; ++w2) v += part[w2][t][k];
-      dq[((int64_t)q * lq + i0 + t) * dim + k] = v;
+  for (int cc = 0; cc < CPL; ++cc) {
+    const int k = 8 * (c + 16 * cc);
+    if (k < dim) {
+      *reinterpret_cast<f32x4*>(dst + k) = f32x4{acc[cc][0], acc[cc][1], acc[cc][2], acc[cc][3]};
+      *reinterpret_cast<f32x4*>(dst + k + 4) = f32x4{acc[cc][4], acc[cc][5], acc[cc][6], acc[cc][7]};
     }
   }
 }
 
-constexpr int kGdThreads = 1024;
-constexpr int kGdUnroll = 16;
+// dQ, second pass: dq[i] = sum over ranges r = 0, 1, ... of part[r][i] (4 values per thread).
+__global__ void grad_q_reduce_kernel(const float* __restrict__ part, int R, int64_t n4,
+                                     float* __restrict__ dq) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n4) return;
+  const f32x4* p = reinterpret_cast<const f32x4*>(part);
+  f32x4 s = p[i];
+  for (int r = 1; r < R; ++r) s += p[(int64_t)r * n4 + i];
+  reinterpret_cast<f32x4*>(dq)[i] = s;
+}
 
-// dD: one workgroup per document d.  Entry e = q * lq + i selected token a(e) = amax[d][e];
-// keys (a(e) << 14 | e) are bitonic-sorted in LDS, so each token's entries are contiguous and
-// in entry order.  Wave w owns a contiguous range of the document's token rows and walks the
-// entries of those rows as one flat stream, kGdUnroll entries (independent Q-row gathers) at a
-// time, flushing a row's sum when the next row starts and writing zeros for rows no entry
-// selected.  Lane: 2 consecutive columns per 128-column block.
+constexpr int kGdWaves = 8;
+constexpr int kGdThreads = 64 * kGdWaves;
+constexpr int kGdWindow = 512;  // document rows per pass
+constexpr int kGdUnroll = 16;   // entries per gather batch (two batches in flight)
+
+// LDS layout of grad_d_kernel (bytes, each part 16-byte aligned).
+struct GdLds {
+  int sorted, cnt, rs, gcol, total;
+};
+__host__ __device__ inline GdLds gd_lds(int E, int nq) {
+  GdLds l;
+  l.sorted = 0;
+  l.cnt = (2 * E + 15) / 16 * 16;
+  l.rs = l.cnt + kGdWaves * kGdWindow * 4;
+  l.gcol = l.rs + ((kGdWindow + 1) * 4 + 15) / 16 * 16;
+  l.total = l.gcol + (4 * nq + 15) / 16 * 16;
+  return l;
+}
+
+// dD: one workgroup per document d.  Entry e = q * lq + i selected token a(e) = amax[d][e] of
+// the document.  Per window of kGdWindow rows, the entries are sorted by token with a stable
+// counting sort in LDS (per-wave histograms over contiguous entry ranges, a prefix scan, then a
+// ballot-ranked scatter in entry order), so each token's entries are contiguous and in entry
+// order.  Wave w then owns a range of rows balanced by entry count and sums each row over its
+// entries in that order -- deterministic without atomics -- writing zeros for rows nobody
+// selected.  G[:, d] is staged in LDS; the Q rows are gathered kGdUnroll at a time with the
+// next batch in flight.  Lane: 2 consecutive columns per 128-column block.
 template <int CP>
 __global__ __launch_bounds__(kGdThreads) void grad_d_kernel(
     const uint16_t* __restrict__ Q, const int64_t* __restrict__ off, int64_t n_docs,
     int64_t n_tok, int dim, int nq, int lq, uint64_t lq_magic,
-    const uint16_t* __restrict__ amax, const float* __restrict__ G, float* dd, int P) {
-  extern __shared__ uint32_t keys[];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  constexpr int kWaves = kGdThreads / kWave;
-  const int64_t d = blockIdx.x;
+    const uint16_t* __restrict__ amax, const float* __restrict__ G, float* __restrict__ dd) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char gd_smem[];
   const int E = nq * lq;
-  for (int e = tid; e < P; e += kGdThreads)
-    keys[e] = e < E ? ((uint32_t)amax[d * E + e] << 14) | (uint32_t)e : 0xffffffffu;
-  for (int size = 2; size <= P; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      __syncthreads();
-      for (int i = tid; i < P; i += kGdThreads) {
-        const int j = i ^ stride;
-        if (j > i) {
-          const bool up = (i & size) == 0;
-          const uint32_t ki = keys[i], kj = keys[j];
-          if ((ki > kj) == up) {
-            keys[i] = kj;
-            keys[j] = ki;
-          }
-        }
-      }
-    }
-  }
-  __syncthreads();
+  const GdLds L = gd_lds(E, nq);
+  uint16_t* sorted = reinterpret_cast<uint16_t*>(gd_smem + L.sorted);
+  int* cnt = reinterpret_cast<int*>(gd_smem + L.cnt);
+  int* rs = reinterpret_cast<int*>(gd_smem + L.rs);
+  float* gcol = reinterpret_cast<float*>(gd_smem + L.gcol);
+  __shared__ int wave_tot[kGdWaves];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t d = blockIdx.x;
+  const uint16_t* am = amax + d * E;
+  for (int q = tid; q < nq; q += kGdThreads) gcol[q] = G[(int64_t)q * n_docs + d];
 
   const int64_t last_tok = n_tok - 1;
-  int64_t lo_t = off[d], hi_t = off[d + 1];
-  lo_t = lo_t < 0 ? 0 : (lo_t > last_tok ? last_tok : lo_t);
-  hi_t = hi_t <= lo_t ? lo_t + 1 : (hi_t > n_tok ? n_tok : hi_t);
-  const int64_t len = hi_t - lo_t;
-  // this wave's rows [j0, j1)
-  const int64_t rows_per = (len + kWaves - 1) / kWaves;
-  const int64_t j0 = wave * rows_per < len ? wave * rows_per : len;
-  const int64_t j1 = j0 + rows_per < len ? j0 + rows_per : len;
-  if (j0 >= j1) return;
-  auto lower = [&](int64_t j) {  // first sorted position whose token is >= j
-    if (j >= 65536) return E;
-    const uint32_t target = (uint32_t)j << 14;
-    int lo = 0, hi = E;
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (keys[mid] < target)
-        lo = mid + 1;
-      else
-        hi = mid;
-    }
-    return lo;
-  };
-  const int p0 = lower(j0), p1 = lower(j1);
+  int64_t lo = off[d], hi = off[d + 1];
+  lo = lo < 0 ? 0 : (lo > last_tok ? last_tok : lo);
+  hi = hi <= lo ? lo + 1 : (hi > n_tok ? n_tok : hi);
+  const int64_t len = hi - lo;
+  // this wave's entries [eb, ee): contiguous, whole 64-entry chunks except at the end
+  const int epw = ((E + kGdWaves - 1) / kGdWaves + 63) / 64 * 64;
+  const int eb = wave * epw < E ? wave * epw : E;
+  const int ee = eb + epw < E ? eb + epw : E;
+  const uint64_t lt_mask = (1ull << lane) - 1ull;
 
-  float acc[CP][2];
-  auto zero_acc = [&]() {
+  for (int64_t w0 = 0; w0 < len; w0 += kGdWindow) {
+    const int Wn = (int)(len - w0 < kGdWindow ? len - w0 : kGdWindow);
+    int nbits = 0;
+    while ((1 << nbits) < Wn) ++nbits;
+    for (int k = lane; k < Wn; k += 64) cnt[wave * kGdWindow + k] = 0;
+    __syncthreads();
+    // per-wave histogram of the window's tokens
+    for (int e = eb + lane; e < ee; e += 64) {
+      const int key = (int)am[e] - (int)w0;
+      if (key >= 0 && key < Wn) atomicAdd(&cnt[wave * kGdWindow + key], 1);
+    }
+    __syncthreads();
+    // exclusive scan over (token, wave) in token-major order; thread t owns token t
+    {
+      int tot = 0;
+      if (tid < Wn)
+        for (int w = 0; w < kGdWaves; ++w) tot += cnt[w * kGdWindow + tid];
+      int incl = tot;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o);
+        if (lane >= o) incl += y;
+      }
+      if (lane == 63) wave_tot[wave] = incl;
+      __syncthreads();
+      int before = 0;
+      for (int w = 0; w < wave; ++w) before += wave_tot[w];
+      const int excl = before + incl - tot;
+      if (tid < Wn) {
+        int run = excl;
+        for (int w = 0; w < kGdWaves; ++w) {
+          const int c = cnt[w * kGdWindow + tid];
+          cnt[w * kGdWindow + tid] = run;
+          run += c;
+        }
+        rs[tid] = excl;
+        if (tid == Wn - 1) rs[Wn] = excl + tot;
+      }
+    }
+    __syncthreads();
+    // stable scatter: in entry order within the wave, ranked among equal tokens by ballots
+    for (int base = eb; base < ee; base += 64) {
+      const int e = base + lane;
+      int key = -1;
+      if (e < ee) key = (int)am[e] - (int)w0;
+      const bool valid = key >= 0 && key < Wn;
+      uint64_t peers = __ballot(valid);
+      for (int b = 0; b < nbits; ++b) {
+        const bool bit = valid && ((key >> b) & 1);
+        const uint64_t m = __ballot(bit);
+        peers &= bit ? m : ~m;
+      }
+      if (valid) {
+        const int rank = __popcll(peers & lt_mask);
+        const int n = __popcll(peers);
+        const int start = cnt[wave * kGdWindow + key];
+        sorted[start + rank] = (uint16_t)e;
+        if (rank == 0) cnt[wave * kGdWindow + key] = start + n;
+      }
+    }
+    __syncthreads();
+
+    // walk: rows [r0, r1) of this wave, balanced by entry count
+    const int total = rs[Wn];
+    auto first_row_at = [&](int target) {  // first row k with rs[k] >= target
+      int a = 0, b = Wn;
+      while (a < b) {
+        const int m = (a + b) >> 1;
+        if (rs[m] < target)
+          a = m + 1;
+        else
+          b = m;
+      }
+      return a;
+    };
+    const int r0 = wave == 0 ? 0 : first_row_at((int)(((int64_t)total * wave + kGdWaves - 1) / kGdWaves));
+    const int r1 = wave == kGdWaves - 1 ? Wn
+                                       : first_row_at((int)(((int64_t)total * (wave + 1) + kGdWaves - 1) / kGdWaves));
+    float acc[CP][2];
 #pragma unroll
     for (int cc = 0; cc < CP; ++cc) acc[cc][0] = acc[cc][1] = 0.f;
-  };
-  auto write_row = [&](int64_t j) {
-#pragma unroll
-    for (int cc = 0; cc < CP; ++cc) {
-      const int c = 2 * lane + 128 * cc;
-      if (c < dim)
-        *reinterpret_cast<float2*>(dd + (lo_t + j) * dim + c) = make_float2(acc[cc][0], acc[cc][1]);
-    }
-  };
-  zero_acc();
-  int64_t cur = j0;  // row being accumulated; rows < cur are written
-  for (int p = p0; p < p1; p += kGdUnroll) {
-    uint32_t kk[kGdUnroll];
-    float g[kGdUnroll];
-    uint32_t w[kGdUnroll][CP];
-#pragma unroll
-    for (int u = 0; u < kGdUnroll; ++u) {
-      kk[u] = p + u < p1 ? keys[p + u] : 0xffffffffu;
-      const uint32_t e = kk[u] & 0x3fffu;
-      const uint32_t qq = (uint32_t)(((uint64_t)e * lq_magic) >> 32);
-      g[u] = p + u < p1 ? G[(int64_t)qq * n_docs + d] : 0.f;
+    int cur = r0;
+    int cur_end = r0 < r1 ? rs[r0 + 1] : 0;
+    float* drow = dd + (lo + w0) * dim;
+    auto flush = [&]() {
 #pragma unroll
       for (int cc = 0; cc < CP; ++cc) {
         const int c = 2 * lane + 128 * cc;
-        w[u][cc] = (p + u < p1 && c < dim)
-                       ? *reinterpret_cast<const uint32_t*>(Q + (int64_t)e * dim + c)
-                       : 0u;
+        if (c < dim)
+          *reinterpret_cast<float2*>(drow + (int64_t)cur * dim + c) = make_float2(acc[cc][0], acc[cc][1]);
+        acc[cc][0] = acc[cc][1] = 0.f;
       }
-    }
+      ++cur;
+      cur_end = cur < r1 ? rs[cur + 1] : 0;
+    };
+    const int p0 = r0 < r1 ? rs[r0] : 0, p1 = r0 < r1 ? rs[r1] : 0;
+    float gA[kGdUnroll], gB[kGdUnroll];
+    uint32_t wA[kGdUnroll][CP], wB[kGdUnroll][CP];
+    auto gather = [&](int p, float (&g)[kGdUnroll], uint32_t (&w)[kGdUnroll][CP]) {
 #pragma unroll
-    for (int u = 0; u < kGdUnroll; ++u) {
-      if (p + u < p1) {
-        const int64_t j = kk[u] >> 14;
-        while (cur < j) {  // finish the current row, zero-fill rows nobody selected
-          write_row(cur);
-          zero_acc();
-          ++cur;
-        }
+      for (int u = 0; u < kGdUnroll; ++u) {
+        const bool ok = p + u < p1;
+        const uint32_t e = ok ? sorted[p + u] : 0u;
+        const uint32_t qq = (uint32_t)(((uint64_t)e * lq_magic) >> 32);
+        g[u] = ok ? gcol[qq] : 0.f;
 #pragma unroll
         for (int cc = 0; cc < CP; ++cc) {
-          acc[cc][0] += g[u] * bf16_lo(w[u][cc]);
-          acc[cc][1] += g[u] * bf16_hi(w[u][cc]);
+          const int c = 2 * lane + 128 * cc;
+          w[u][cc] = (ok && c < dim) ? *reinterpret_cast<const uint32_t*>(Q + (int64_t)e * dim + c) : 0u;
         }
       }
+    };
+    if (p0 < p1) gather(p0, gA, wA);
+    for (int p = p0; p < p1; p += kGdUnroll) {
+      if (p + kGdUnroll < p1) gather(p + kGdUnroll, gB, wB);
+#pragma unroll
+      for (int u = 0; u < kGdUnroll; ++u) {
+        if (p + u < p1) {
+          while (p + u >= cur_end && cur < r1) flush();  // earlier rows are complete
+#pragma unroll
+          for (int cc = 0; cc < CP; ++cc) {
+            acc[cc][0] += gA[u] * bf16_lo(wA[u][cc]);
+            acc[cc][1] += gA[u] * bf16_hi(wA[u][cc]);
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kGdUnroll; ++u) {
+        gA[u] = gB[u];
+#pragma unroll
+        for (int cc = 0; cc < CP; ++cc) wA[u][cc] = wB[u][cc];
+      }
     }
-  }
-  while (cur < j1) {
-    write_row(cur);
-    zero_acc();
-    ++cur;
+    while (cur < r1) flush();
+    __syncthreads();  // the window's LDS is reused by the next one
   }
 }
 
@@ -357,16 +439,33 @@ hipError_t launch_infonce(const float* S, int nq, int64_t n_docs, const int32_t*
   return hipGetLastError();
 }
 
+int grad_q_ranges(int64_t n_docs, int64_t n_tok, int64_t E, int dim) {
+  // about 2 MiB of document rows per range (an XCD's L2 holds its ranges' rows), at most 32
+  // ranges and 64 MiB of partial sums
+  int64_t R = (n_tok * dim * 2 + (2 << 20) - 1) / (2 << 20);
+  const int64_t by_mem = ((int64_t)64 << 20) / (E * dim * 4 > 0 ? E * dim * 4 : 1);
+  if (R > by_mem) R = by_mem;
+  if (R > 32) R = 32;
+  if (R > n_docs) R = n_docs;
+  return R < 1 ? 1 : (int)R;
+}
+
 hipError_t launch_grad_q(const uint16_t* d_tok, const int64_t* off, int64_t n_docs, int64_t n_tok,
-                         int dim, int nq, int lq, const uint16_t* amax, const float* G, float* dq,
-                         hipStream_t stream) {
-  const unsigned blocks = (unsigned)((int64_t)nq * ((lq + 3) / 4));
+                         int dim, int nq, int lq, const uint16_t* amax, const float* G,
+                         float* part, float* dq, hipStream_t stream) {
+  const int64_t E = (int64_t)nq * lq;
+  const int R = grad_q_ranges(n_docs, n_tok, E, dim);
+  const int n_groups = (int)((E + kGqEntries - 1) / kGqEntries);
+  const unsigned blocks = (unsigned)((int64_t)n_groups * R);
   if (dim <= 128)
-    hipLaunchKernelGGL(grad_q_kernel<1>, dim3(blocks), dim3(64 * kGqWaves), 0, stream, d_tok, off,
-                       n_docs, n_tok, dim, nq, lq, amax, G, dq);
+    hipLaunchKernelGGL(grad_q_part_kernel<1>, dim3(blocks), dim3(kGqThreads), 0, stream, d_tok,
+                       off, n_docs, n_tok, dim, nq, lq, amax, G, part, n_groups, R);
   else
-    hipLaunchKernelGGL(grad_q_kernel<2>, dim3(blocks), dim3(64 * kGqWaves), 0, stream, d_tok, off,
-                       n_docs, n_tok, dim, nq, lq, amax, G, dq);
+    hipLaunchKernelGGL(grad_q_part_kernel<2>, dim3(blocks), dim3(kGqThreads), 0, stream, d_tok,
+                       off, n_docs, n_tok, dim, nq, lq, amax, G, part, n_groups, R);
+  const int64_t n4 = E * dim / 4;
+  hipLaunchKernelGGL(grad_q_reduce_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0,
+                     stream, part, R, n4, dq);
   return hipGetLastError();
 }
 
@@ -374,18 +473,21 @@ hipError_t launch_grad_d(const uint16_t* q, const int64_t* off, int64_t n_docs, 
                          int dim, int nq, int lq, const uint16_t* amax, const float* G, float* dd,
                          hipStream_t stream) {
   const int E = nq * lq;
-  int P = 1;
-  while (P < E) P <<= 1;
-  const size_t lds = (size_t)P * sizeof(uint32_t);
+  const int lds = gd_lds(E, nq).total;
   // floor(e / lq) = (e * ceil(2^32 / lq)) >> 32 for e < 2^14 and lq <= 128: the product
   // overshoots e / lq by less than e / 2^32 < 2^-18, below the 1 / lq gap to the next integer.
   const uint64_t magic = (0x100000000ull + (uint64_t)lq - 1) / (uint64_t)lq;
+  if (lds > 65536) {  // beyond the default dynamic LDS limit (large nq * lq only)
+    const void* fn = dim <= 128 ? (const void*)grad_d_kernel<1> : (const void*)grad_d_kernel<2>;
+    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+  }
   if (dim <= 128)
     hipLaunchKernelGGL(grad_d_kernel<1>, dim3((unsigned)n_docs), dim3(kGdThreads), lds, stream,
-                       q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, P);
+                       q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd);
   else
     hipLaunchKernelGGL(grad_d_kernel<2>, dim3((unsigned)n_docs), dim3(kGdThreads), lds, stream,
-                       q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, P);
+                       q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd);
   return hipGetLastError();
 }
 
