@@ -14,8 +14,9 @@
 //   * C layout (32x32): lane l holds column l % 32 (a query slot) and the 16 rows
 //     8 (i / 4) + 4 (l / 32) + i % 4, i = 0..15 (document tokens).  The plain score folds each
 //     tile's 16 values into one running max per lane with v_max3 (8 instructions per tile and
-//     block); the argmax variant keeps a running (max, tile) per row register.  At the end of a
-//     document the two half-waves are combined and the slot maxima summed per query.
+//     block); the argmax variant also keeps the tile of the running maximum and a copy of that
+//     tile's 16 values, from which the row is recovered at the end of the document.  There the
+//     two half-waves are combined and the slot maxima summed per query.
 //   * Workgroup = 4 waves on 4 query sets, all consuming the same stream of document tiles,
 //     which the workgroup stages through LDS (double-buffered, one stage in flight).  Workgroups
 //     sharing a document range are mapped onto the same XCD and start together, so the range is
@@ -254,18 +255,21 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_occupancy<KS, ARGMAX>())) void ma
     }
   };
 
-  // running state: plain -> rmx[b] (one max per lane and block); argmax -> (rm, ra) per row
-  // register (ra = tile index of the maximum)
-  constexpr int kRows = ARGMAX ? 16 : 1;
-  float rm[NB][kRows];
-  int ra[NB][kRows];
+  // Running state per lane and block.  Plain: rm[b][0], the maximum so far.  Argmax: rm[b][0]
+  // and the tile bt[b] holding it, plus that tile's 16 row values bv[b][:] (copied whenever a
+  // later tile's maximum is strictly larger, so the earliest tile keeps ties); the row within
+  // the tile is found once, at the end of the document.
+  constexpr int kVals = ARGMAX ? 16 : 1;
+  float rm[NB][1];
+  int bt[NB];
+  float bv[NB][kVals];
 #pragma unroll
-  for (int b = 0; b < NB; ++b)
+  for (int b = 0; b < NB; ++b) {
+    rm[b][0] = -__builtin_huge_valf();
+    bt[b] = 0;
 #pragma unroll
-    for (int r = 0; r < kRows; ++r) {
-      rm[b][r] = -__builtin_huge_valf();
-      ra[b][r] = 0;
-    }
+    for (int r = 0; r < kVals; ++r) bv[b][r] = 0.f;
+  }
   const int64_t n_entries = (int64_t)a.nq * a.lq;
   const int n_wg_q = (a.nq - qwg) < WPW * a.qpw ? (a.nq - qwg) : WPW * a.qpw;
   const int n_wg_e = n_wg_q * a.lq;
@@ -302,19 +306,17 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_occupancy<KS, ARGMAX>())) void ma
         }
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
+          float m = fmaxf(acc[b][0], acc[b][1]);  // this tile's maximum over the lane's rows
+#pragma unroll
+          for (int r = 2; r < 16; r += 2) m = fmaxf(fmaxf(m, acc[b][r]), acc[b][r + 1]);
           if (ARGMAX) {
+            const bool gt = m > rm[b][0];  // strict: the earlier tile keeps ties
+            rm[b][0] = gt ? m : rm[b][0];
+            bt[b] = gt ? t : bt[b];
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const float v = acc[b][r];
-              const bool gt = v > rm[b][r];  // strict: the earlier tile keeps ties
-              rm[b][r] = gt ? v : rm[b][r];
-              ra[b][r] = gt ? t : ra[b][r];
-            }
+            for (int r = 0; r < 16; ++r) bv[b][r] = gt ? acc[b][r] : bv[b][r];
           } else {
-            float m = rm[b][0];
-#pragma unroll
-            for (int r = 0; r < 16; r += 2) m = fmaxf(fmaxf(m, acc[b][r]), acc[b][r + 1]);
-            rm[b][0] = m;
+            rm[b][0] = fmaxf(rm[b][0], m);
           }
         }
         if (last) {  // last tile of the document: reduce over rows and half-waves, emit
@@ -323,31 +325,20 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_occupancy<KS, ARGMAX>())) void ma
           for (int b = 0; b < NB; ++b) {
             float m;
             if (ARGMAX) {
-              // best (value, token) of this lane's 16 row registers, lower token on ties
-              // (reduced in place: the running state is reset right after)
-#pragma unroll
-              for (int r = 0; r < 16; ++r) ra[b][r] = ra[b][r] * 32 + 8 * (r >> 2) + row_base + (r & 3);
-#pragma unroll
-              for (int w = 1; w < 16; w <<= 1)
-#pragma unroll
-                for (int r = 0; r < 16; r += 2 * w) {
-                  const bool tk = beats(rm[b][r + w], ra[b][r + w], rm[b][r], ra[b][r]);
-                  rm[b][r] = tk ? rm[b][r + w] : rm[b][r];
-                  ra[b][r] = tk ? ra[b][r + w] : ra[b][r];
-                }
+              // lowest row of the best tile holding the maximum (rows ascend with r), then the
+              // lower token of the two half-waves
               m = rm[b][0];
-              int jx = ra[b][0];
+              int jr = 15;
+#pragma unroll
+              for (int r = 14; r >= 0; --r) jr = bv[b][r] == m ? r : jr;
+              int jx = bt[b] * 32 + 8 * (jr >> 2) + row_base + (jr & 3);
               const float om = __shfl_xor(m, 32);
               const int oj = __shfl_xor(jx, 32);
               const bool tk = beats(om, oj, m, jx);
               m = tk ? om : m;
               jx = tk ? oj : jx;
               if (half == 0 && slot_row[b] >= 0) res_amax[buf][j][slot_row[b]] = (uint16_t)jx;
-#pragma unroll
-              for (int r = 0; r < 16; ++r) {
-                rm[b][r] = -__builtin_huge_valf();
-                ra[b][r] = 0;
-              }
+              rm[b][0] = -__builtin_huge_valf();
             } else {
               m = fmaxf(rm[b][0], __shfl_xor(rm[b][0], 32));
               rm[b][0] = -__builtin_huge_valf();
@@ -449,8 +440,7 @@ hipError_t launch_t(const MaxsimPlan& plan, const MaxsimArgs& args, hipStream_t 
 
 // Variants by k-steps of 16 (dim <= 16 KS).  Query slots per wave: 128 (plain, dim <= 64),
 // 64 (plain, dim 128 and 256; argmax, dim <= 128), 32 (argmax, dim 256) -- what fits two
-// waves per SIMD in 256 registers; the argmax variants keep a running (max, tile) per row
-// register.
+// waves per SIMD in 256 registers next to the argmax variants' 18 state registers per block.
 hipError_t launch_variant(const MaxsimPlan& plan, const MaxsimArgs& args, bool argmax,
                           hipStream_t stream) {
   if (argmax) {
