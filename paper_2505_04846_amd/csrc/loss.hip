@@ -227,41 +227,53 @@ __global__ void grad_q_reduce_kernel(const float* __restrict__ part, int R, int6
   reinterpret_cast<f32x4*>(dq)[i] = s;
 }
 
-constexpr int kGdWaves = 8;
+constexpr int kGdWaves = 16;
 constexpr int kGdThreads = 64 * kGdWaves;
-constexpr int kGdWindow = 512;  // document rows per pass
-constexpr int kGdUnroll = 16;   // entries per gather batch (two batches in flight)
+constexpr int kGdCols = 32;        // dD columns a thread owns (4 chunks of 8)
+constexpr int kGdBatch = 4;        // entries whose Q rows a thread loads at once
+constexpr int kGdMaxStageQ = 4096;  // G[:, d] is staged in LDS when nq is at most this
+
+// TPR threads own one dD row (chunk c of the row, 8 columns, belongs to thread c % TPR), so a
+// pass covers RPP = 1024 / TPR rows of a document.
+__host__ __device__ inline int gd_tpr(int dim) { return dim <= 64 ? 2 : dim <= 128 ? 4 : 8; }
 
 // LDS layout of grad_d_kernel (bytes, each part 16-byte aligned).
 struct GdLds {
-  int sorted, cnt, rs, gcol, total;
+  int keys, sorted, cnt, rs, gcol, total;
 };
-__host__ __device__ inline GdLds gd_lds(int E, int nq) {
+__host__ __device__ inline GdLds gd_lds(int E, int nq, int dim) {
+  const int rpp = kGdThreads / gd_tpr(dim);
   GdLds l;
-  l.sorted = 0;
-  l.cnt = (2 * E + 15) / 16 * 16;
-  l.rs = l.cnt + kGdWaves * kGdWindow * 4;
-  l.gcol = l.rs + ((kGdWindow + 1) * 4 + 15) / 16 * 16;
-  l.total = l.gcol + (4 * nq + 15) / 16 * 16;
+  l.keys = 0;  // the document's argmax entries, staged once
+  l.sorted = (2 * E + 15) / 16 * 16;
+  l.cnt = l.sorted + (2 * E + 15) / 16 * 16;
+  l.rs = l.cnt + kGdWaves * rpp * 4;
+  l.gcol = l.rs + ((rpp + 1) * 4 + 15) / 16 * 16;
+  l.total = l.gcol + (nq <= kGdMaxStageQ ? (4 * nq + 15) / 16 * 16 : 0);
   return l;
 }
 
 // dD: one workgroup per document d.  Entry e = q * lq + i selected token a(e) = amax[d][e] of
-// the document.  Per window of kGdWindow rows, the entries are sorted by token with a stable
-// counting sort in LDS (per-wave histograms over contiguous entry ranges, a prefix scan, then a
-// ballot-ranked scatter in entry order), so each token's entries are contiguous and in entry
-// order.  Wave w then owns a range of rows balanced by entry count and sums each row over its
-// entries in that order -- deterministic without atomics -- writing zeros for rows nobody
-// selected.  G[:, d] is staged in LDS; the Q rows are gathered kGdUnroll at a time with the
-// next batch in flight.  Lane: 2 consecutive columns per 128-column block.
-template <int CP>
+// the document; dD[j] = sum over the entries with a(e) = j, in entry order, of G[q,d] Q[e].
+// The argmax entries (and G[:, d]) are staged in LDS.  Per pass over RPP rows:
+//   1. a stable counting sort of the entries by token -- per-wave histograms over contiguous
+//      entry ranges, a prefix scan, a ballot-ranked scatter in entry order -- gives each row
+//      its entries, in entry order;
+//   2. the TPR threads of row j keep its columns in registers and walk its entries, kGdBatch at
+//      a time, gathering their Q rows straight from L2 (the TPR threads of a row read 16 * TPR
+//      contiguous bytes per load);
+//   3. each row is written once -- zeros for rows nobody selected.
+// Deterministic: every row sums its entries in entry order, with no atomics on floats.
+template <int TPR>
 __global__ __launch_bounds__(kGdThreads) void grad_d_kernel(
     const uint16_t* __restrict__ Q, const int64_t* __restrict__ off, int64_t n_docs,
     int64_t n_tok, int dim, int nq, int lq, uint64_t lq_magic,
     const uint16_t* __restrict__ amax, const float* __restrict__ G, float* __restrict__ dd) {
   extern __shared__ __attribute__((aligned(16))) unsigned char gd_smem[];
+  constexpr int RPP = kGdThreads / TPR;
   const int E = nq * lq;
-  const GdLds L = gd_lds(E, nq);
+  const GdLds L = gd_lds(E, nq, dim);
+  uint16_t* am = reinterpret_cast<uint16_t*>(gd_smem + L.keys);
   uint16_t* sorted = reinterpret_cast<uint16_t*>(gd_smem + L.sorted);
   int* cnt = reinterpret_cast<int*>(gd_smem + L.cnt);
   int* rs = reinterpret_cast<int*>(gd_smem + L.rs);
@@ -270,8 +282,16 @@ __global__ __launch_bounds__(kGdThreads) void grad_d_kernel(
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t d = blockIdx.x;
-  const uint16_t* am = amax + d * E;
-  for (int q = tid; q < nq; q += kGdThreads) gcol[q] = G[(int64_t)q * n_docs + d];
+  const bool g_staged = nq <= kGdMaxStageQ;
+  {
+    const uint16_t* src = amax + d * E;
+    const int nvec = (E % 8 == 0) ? E / 8 : 0;  // 16-byte loads need 16-byte aligned rows
+    for (int i = tid; i < nvec; i += kGdThreads)
+      reinterpret_cast<u32x4*>(am)[i] = load16(src + 8 * i);
+    for (int e = 8 * nvec + tid; e < E; e += kGdThreads) am[e] = src[e];
+    if (g_staged)
+      for (int q = tid; q < nq; q += kGdThreads) gcol[q] = G[(int64_t)q * n_docs + d];
+  }
 
   const int64_t last_tok = n_tok - 1;
   int64_t lo = off[d], hi = off[d + 1];
@@ -283,24 +303,26 @@ __global__ __launch_bounds__(kGdThreads) void grad_d_kernel(
   const int eb = wave * epw < E ? wave * epw : E;
   const int ee = eb + epw < E ? eb + epw : E;
   const uint64_t lt_mask = (1ull << lane) - 1ull;
+  const int j = tid / TPR;          // row of this thread within the pass
+  const int cp = tid - j * TPR;     // its chunk phase: chunks cp, cp + TPR, ...
 
-  for (int64_t w0 = 0; w0 < len; w0 += kGdWindow) {
-    const int Wn = (int)(len - w0 < kGdWindow ? len - w0 : kGdWindow);
+  for (int64_t w0 = 0; w0 < len; w0 += RPP) {
+    const int Wn = (int)(len - w0 < RPP ? len - w0 : RPP);
     int nbits = 0;
     while ((1 << nbits) < Wn) ++nbits;
-    for (int k = lane; k < Wn; k += 64) cnt[wave * kGdWindow + k] = 0;
+    for (int k = lane; k < Wn; k += 64) cnt[wave * RPP + k] = 0;
     __syncthreads();
-    // per-wave histogram of the window's tokens
+    // per-wave histogram of the pass's tokens
     for (int e = eb + lane; e < ee; e += 64) {
       const int key = (int)am[e] - (int)w0;
-      if (key >= 0 && key < Wn) atomicAdd(&cnt[wave * kGdWindow + key], 1);
+      if (key >= 0 && key < Wn) atomicAdd(&cnt[wave * RPP + key], 1);
     }
     __syncthreads();
     // exclusive scan over (token, wave) in token-major order; thread t owns token t
     {
       int tot = 0;
       if (tid < Wn)
-        for (int w = 0; w < kGdWaves; ++w) tot += cnt[w * kGdWindow + tid];
+        for (int w = 0; w < kGdWaves; ++w) tot += cnt[w * RPP + tid];
       int incl = tot;
 #pragma unroll
       for (int o = 1; o < 64; o <<= 1) {
@@ -315,8 +337,8 @@ __global__ __launch_bounds__(kGdThreads) void grad_d_kernel(
       if (tid < Wn) {
         int run = excl;
         for (int w = 0; w < kGdWaves; ++w) {
-          const int c = cnt[w * kGdWindow + tid];
-          cnt[w * kGdWindow + tid] = run;
+          const int c = cnt[w * RPP + tid];
+          cnt[w * RPP + tid] = run;
           run += c;
         }
         rs[tid] = excl;
@@ -339,86 +361,63 @@ __global__ __launch_bounds__(kGdThreads) void grad_d_kernel(
       if (valid) {
         const int rank = __popcll(peers & lt_mask);
         const int n = __popcll(peers);
-        const int start = cnt[wave * kGdWindow + key];
+        const int start = cnt[wave * RPP + key];
         sorted[start + rank] = (uint16_t)e;
-        if (rank == 0) cnt[wave * kGdWindow + key] = start + n;
+        if (rank == 0) cnt[wave * RPP + key] = start + n;
       }
     }
     __syncthreads();
 
-    // walk: rows [r0, r1) of this wave, balanced by entry count
-    const int total = rs[Wn];
-    auto first_row_at = [&](int target) {  // first row k with rs[k] >= target
-      int a = 0, b = Wn;
-      while (a < b) {
-        const int m = (a + b) >> 1;
-        if (rs[m] < target)
-          a = m + 1;
-        else
-          b = m;
-      }
-      return a;
-    };
-    const int r0 = wave == 0 ? 0 : first_row_at((int)(((int64_t)total * wave + kGdWaves - 1) / kGdWaves));
-    const int r1 = wave == kGdWaves - 1 ? Wn
-                                       : first_row_at((int)(((int64_t)total * (wave + 1) + kGdWaves - 1) / kGdWaves));
-    float acc[CP][2];
+    // row j's entries, kGdBatch at a time (absent entries repeat a valid one with weight 0)
+    float acc[kGdCols];
 #pragma unroll
-    for (int cc = 0; cc < CP; ++cc) acc[cc][0] = acc[cc][1] = 0.f;
-    int cur = r0;
-    int cur_end = r0 < r1 ? rs[r0 + 1] : 0;
-    float* drow = dd + (lo + w0) * dim;
-    auto flush = [&]() {
+    for (int v = 0; v < kGdCols; ++v) acc[v] = 0.f;
+    if (j < Wn) {
+      const int p_end = rs[j + 1];
+      for (int p = rs[j]; p < p_end; p += kGdBatch) {
+        u32x4 w[kGdBatch][4];
+        float g[kGdBatch];
 #pragma unroll
-      for (int cc = 0; cc < CP; ++cc) {
-        const int c = 2 * lane + 128 * cc;
-        if (c < dim)
-          *reinterpret_cast<float2*>(drow + (int64_t)cur * dim + c) = make_float2(acc[cc][0], acc[cc][1]);
-        acc[cc][0] = acc[cc][1] = 0.f;
-      }
-      ++cur;
-      cur_end = cur < r1 ? rs[cur + 1] : 0;
-    };
-    const int p0 = r0 < r1 ? rs[r0] : 0, p1 = r0 < r1 ? rs[r1] : 0;
-    float gA[kGdUnroll], gB[kGdUnroll];
-    uint32_t wA[kGdUnroll][CP], wB[kGdUnroll][CP];
-    auto gather = [&](int p, float (&g)[kGdUnroll], uint32_t (&w)[kGdUnroll][CP]) {
+        for (int b = 0; b < kGdBatch; ++b) {
+          const bool ok = p + b < p_end;
+          const uint32_t e = sorted[ok ? p + b : p];
+          const uint32_t qq = (uint32_t)(((uint64_t)e * lq_magic) >> 32);
+          const float gv = g_staged ? gcol[qq] : G[(int64_t)qq * n_docs + d];
+          g[b] = ok ? gv : 0.f;
+          const uint16_t* qrow = Q + (int64_t)e * dim;
 #pragma unroll
-      for (int u = 0; u < kGdUnroll; ++u) {
-        const bool ok = p + u < p1;
-        const uint32_t e = ok ? sorted[p + u] : 0u;
-        const uint32_t qq = (uint32_t)(((uint64_t)e * lq_magic) >> 32);
-        g[u] = ok ? gcol[qq] : 0.f;
-#pragma unroll
-        for (int cc = 0; cc < CP; ++cc) {
-          const int c = 2 * lane + 128 * cc;
-          w[u][cc] = (ok && c < dim) ? *reinterpret_cast<const uint32_t*>(Q + (int64_t)e * dim + c) : 0u;
-        }
-      }
-    };
-    if (p0 < p1) gather(p0, gA, wA);
-    for (int p = p0; p < p1; p += kGdUnroll) {
-      if (p + kGdUnroll < p1) gather(p + kGdUnroll, gB, wB);
-#pragma unroll
-      for (int u = 0; u < kGdUnroll; ++u) {
-        if (p + u < p1) {
-          while (p + u >= cur_end && cur < r1) flush();  // earlier rows are complete
-#pragma unroll
-          for (int cc = 0; cc < CP; ++cc) {
-            acc[cc][0] += gA[u] * bf16_lo(wA[u][cc]);
-            acc[cc][1] += gA[u] * bf16_hi(wA[u][cc]);
+          for (int i = 0; i < 4; ++i) {
+            const int c = cp + TPR * i;  // chunk: columns 8c .. 8c + 7
+            w[b][i] = 8 * c < dim ? load16(qrow + 8 * c) : u32x4{0u, 0u, 0u, 0u};
           }
         }
+#pragma unroll
+        for (int b = 0; b < kGdBatch; ++b)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            acc[8 * i + 0] += g[b] * bf16_lo(w[b][i].x);
+            acc[8 * i + 1] += g[b] * bf16_hi(w[b][i].x);
+            acc[8 * i + 2] += g[b] * bf16_lo(w[b][i].y);
+            acc[8 * i + 3] += g[b] * bf16_hi(w[b][i].y);
+            acc[8 * i + 4] += g[b] * bf16_lo(w[b][i].z);
+            acc[8 * i + 5] += g[b] * bf16_hi(w[b][i].z);
+            acc[8 * i + 6] += g[b] * bf16_lo(w[b][i].w);
+            acc[8 * i + 7] += g[b] * bf16_hi(w[b][i].w);
+          }
       }
+      float* drow = dd + (lo + w0 + j) * dim;
 #pragma unroll
-      for (int u = 0; u < kGdUnroll; ++u) {
-        gA[u] = gB[u];
-#pragma unroll
-        for (int cc = 0; cc < CP; ++cc) wA[u][cc] = wB[u][cc];
+      for (int i = 0; i < 4; ++i) {
+        const int c = cp + TPR * i;
+        if (8 * c < dim) {
+          *reinterpret_cast<f32x4*>(drow + 8 * c) =
+              f32x4{acc[8 * i], acc[8 * i + 1], acc[8 * i + 2], acc[8 * i + 3]};
+          *reinterpret_cast<f32x4*>(drow + 8 * c + 4) =
+              f32x4{acc[8 * i + 4], acc[8 * i + 5], acc[8 * i + 6], acc[8 * i + 7]};
+        }
       }
     }
-    while (cur < r1) flush();
-    __syncthreads();  // the window's LDS is reused by the next one
+    __syncthreads();  // the pass's LDS is reused by the next one
   }
 }
 
@@ -469,26 +468,33 @@ hipError_t launch_grad_q(const uint16_t* d_tok, const int64_t* off, int64_t n_do
   return hipGetLastError();
 }
 
+template <int TPR>
+hipError_t launch_grad_d_t(const uint16_t* q, const int64_t* off, int64_t n_docs, int64_t n_tok,
+                           int dim, int nq, int lq, uint64_t magic, const uint16_t* amax,
+                           const float* G, float* dd, int lds, hipStream_t stream) {
+  if (lds > 65536) {  // beyond the default dynamic LDS limit (large nq * lq only)
+    const hipError_t e = hipFuncSetAttribute((const void*)grad_d_kernel<TPR>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(grad_d_kernel<TPR>, dim3((unsigned)n_docs), dim3(kGdThreads), lds, stream, q,
+                     off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd);
+  return hipGetLastError();
+}
+
 hipError_t launch_grad_d(const uint16_t* q, const int64_t* off, int64_t n_docs, int64_t n_tok,
                          int dim, int nq, int lq, const uint16_t* amax, const float* G, float* dd,
                          hipStream_t stream) {
   const int E = nq * lq;
-  const int lds = gd_lds(E, nq).total;
+  const int lds = gd_lds(E, nq, dim).total;
   // floor(e / lq) = (e * ceil(2^32 / lq)) >> 32 for e < 2^14 and lq <= 128: the product
   // overshoots e / lq by less than e / 2^32 < 2^-18, below the 1 / lq gap to the next integer.
   const uint64_t magic = (0x100000000ull + (uint64_t)lq - 1) / (uint64_t)lq;
-  if (lds > 65536) {  // beyond the default dynamic LDS limit (large nq * lq only)
-    const void* fn = dim <= 128 ? (const void*)grad_d_kernel<1> : (const void*)grad_d_kernel<2>;
-    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-    if (e != hipSuccess) return e;
+  switch (gd_tpr(dim)) {
+    case 2: return launch_grad_d_t<2>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, lds, stream);
+    case 4: return launch_grad_d_t<4>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, lds, stream);
+    default: return launch_grad_d_t<8>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, lds, stream);
   }
-  if (dim <= 128)
-    hipLaunchKernelGGL(grad_d_kernel<1>, dim3((unsigned)n_docs), dim3(kGdThreads), lds, stream,
-                       q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd);
-  else
-    hipLaunchKernelGGL(grad_d_kernel<2>, dim3((unsigned)n_docs), dim3(kGdThreads), lds, stream,
-                       q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd);
-  return hipGetLastError();
 }
 
 hipError_t launch_scale(float* x, int64_t n, const float* scale, hipStream_t stream) {
