@@ -29,6 +29,8 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBS = 8000.0
+COPY_CALIBRATION_BYTES = 256 << 20  # bytes read (and written) by each calibration copy
+CPU_SAMPLE_SECONDS = 10.0  # the oracle sample is repeated for at least this long
 KERNELS = ("partition", "maxsim", "maxsim_argmax", "topk", "infonce", "grad_q", "grad_d",
            "dense_sample", "dense_scan", "dense_merge")
 
@@ -46,6 +48,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the extra HIP-graph replay timing of the same step")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run a plain 256 MiB device-to-device copy three times (the "
+                         "reference kernel that scales rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     return ap.parse_args()
 
 
@@ -105,11 +110,14 @@ def build_workload(name, dev, scale):
         def cpu_sample():
             import oracle
             bf = lambda t: oracle.decode_bf16(t.view(torch.int16).numpy())
-            t0 = time.perf_counter()
-            oracle.coltrast_li_loss(bf(w["Q"]), bf(w["D"]), w["off"].numpy(), w["pos"].numpy(),
-                                    scale)
+            args = (bf(w["Q"]), bf(w["D"]), w["off"].numpy(), w["pos"].numpy(), scale)
+            reps, t0 = 0, time.perf_counter()
+            while reps == 0 or time.perf_counter() - t0 < CPU_SAMPLE_SECONDS:
+                oracle.coltrast_li_loss(*args)
+                reps += 1
             dt = time.perf_counter() - t0
-            return nq * n_docs / dt, "the full workload once: loss, dQ and dD (64 x 512 pairs)"
+            return reps * nq * n_docs / dt, (f"the full workload {reps} times: loss, dQ and dD "
+                                             f"({nq} x {n_docs} pairs each)")
 
         cfg = {"workload": "coltrast_step", "nq": nq, "lq": lq, "n_docs": n_docs, "ld": 256,
                "dim": dim, "hard_negatives_per_query": 7, "logit_scale": scale}
@@ -202,6 +210,13 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_calibration:
+        src = torch.ones(COPY_CALIBRATION_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     W = build_workload(args.workload, dev, args.logit_scale)
     print(f"[bench] workload {args.workload} ready", file=sys.stderr, flush=True)
 
