@@ -15,10 +15,10 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 constexpr int kMaxRanges = 1 << 16;   // upper bound on document ranges (partition table size)
 
 struct MaxsimPlan {
-  int ks;          // k-steps of 32 (dim <= 32 * ks)
-  int nb;          // 16-column query-slot blocks per wave
+  int ks;          // k-steps of 16 (dim <= 16 * ks)
+  int nb;          // 32-slot query blocks per wave
   int wpw;         // waves per workgroup
-  int lqp;         // query slots per query (lq rounded up to 16)
+  int lqp;         // query slots per query (lq rounded up to 32)
   int qpw;         // queries per wave
   int n_qgroups;   // workgroups along the query axis
   int n_ranges;    // document ranges (workgroups along the document axis)
