@@ -138,7 +138,6 @@ __global__ __launch_bounds__(kRowThreads) void infonce_kernel(const float* __res
 constexpr int kGqWaves = 4;
 constexpr int kGqThreads = 64 * kGqWaves;
 constexpr int kGqEntries = 4 * kGqWaves;  // (q, i) entries per workgroup: 16 lanes each
-constexpr int kGqUnroll = 8;
 
 // dQ, first pass: workgroup (r, g) sums, for the 16 entries e = q * lq + i of group g, the
 // gathered rows G[q,d] * D[token a(q,i,d)] over the documents of range r.  Ranges are placed on
@@ -157,8 +156,6 @@ __global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
   const int64_t E = (int64_t)nq * lq;
   const int64_t e = (int64_t)grp * kGqEntries + wave * 4 + (lane >> 4);
   const bool active = e < E;
-  const int64_t ee = active ? e : 0;
-  const int64_t q = ee / lq;
   const int c = lane & 15;
   const int64_t d0 = n_docs * r / R, d1 = n_docs * (r + 1) / R;
   const int64_t last_tok = n_tok - 1;
@@ -169,40 +166,59 @@ __global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
 #pragma unroll
     for (int v = 0; v < 8; ++v) acc[cc][v] = 0.f;
 
-  for (int64_t db = d0; db < d1; db += kGqUnroll) {
-    float g[kGqUnroll];
-    int64_t row[kGqUnroll];
+  // Documents in chunks of 32.  First, lane l loads the row index and weight of two of the
+  // wave's four entries (2 (l >> 5) and the next) against document l & 31 of the chunk -- one
+  // round trip for the chunk's metadata; then each 16-lane group gathers its entry's rows,
+  // 16 documents at a time, taking the metadata from the lanes that loaded it.
+  const int mu = lane & 31, mh = lane >> 5;
+  const int k = lane >> 4;  // this lane's entry within the wave
+  for (int64_t db = d0; db < d1; db += 32) {
+    const int64_t dm = db + mu;
+    const bool okd = dm < d1;
+    int64_t base = okd ? off[dm] : 0;
+    base = base < 0 ? 0 : (base > last_tok ? last_tok : base);
+    int rowm[2];
+    float gm[2];
 #pragma unroll
-    for (int u = 0; u < kGqUnroll; ++u) {
-      const int64_t d = db + u;
-      const bool ok = d < d1;
-      g[u] = ok ? G[q * n_docs + d] : 0.f;
-      int64_t base = ok ? off[d] : 0;
-      base = base < 0 ? 0 : (base > last_tok ? last_tok : base);
-      const int64_t rr = base + (ok ? amax[d * E + ee] : 0);
-      row[u] = rr > last_tok ? last_tok : rr;
+    for (int t = 0; t < 2; ++t) {
+      const int64_t ek = (int64_t)grp * kGqEntries + wave * 4 + 2 * mh + t;
+      const bool ok = okd && ek < E;
+      const int64_t rr = base + (ok ? amax[dm * E + ek] : 0);
+      rowm[t] = (int)(rr > last_tok ? last_tok : rr);
+      gm[t] = ok ? G[(ek / lq) * n_docs + dm] : 0.f;
     }
-    u32x4 w[kGqUnroll][CPL];
 #pragma unroll
-    for (int u = 0; u < kGqUnroll; ++u)
+    for (int half = 0; half < 2; ++half) {
+      if (db + 16 * half >= d1) break;  // uniform
+      u32x4 w[16][CPL];
+      float g[16];
 #pragma unroll
-      for (int cc = 0; cc < CPL; ++cc) {
-        const int k = 8 * (c + 16 * cc);
-        w[u][cc] = k < dim ? load16(D + row[u] * dim + k) : u32x4{0u, 0u, 0u, 0u};
+      for (int uu = 0; uu < 16; ++uu) {
+        const int src = 16 * half + uu + 32 * (k >> 1);
+        const int rA = __shfl(rowm[0], src), rB = __shfl(rowm[1], src);
+        const float gA = __shfl(gm[0], src), gB = __shfl(gm[1], src);
+        const int64_t row = (k & 1) ? rB : rA;
+        g[uu] = (k & 1) ? gB : gA;
+#pragma unroll
+        for (int cc = 0; cc < CPL; ++cc) {
+          const int kk = 8 * (c + 16 * cc);
+          w[uu][cc] = kk < dim ? load16(D + row * dim + kk) : u32x4{0u, 0u, 0u, 0u};
+        }
       }
 #pragma unroll
-    for (int u = 0; u < kGqUnroll; ++u)
+      for (int uu = 0; uu < 16; ++uu)
 #pragma unroll
-      for (int cc = 0; cc < CPL; ++cc) {
-        acc[cc][0] += g[u] * bf16_lo(w[u][cc].x);
-        acc[cc][1] += g[u] * bf16_hi(w[u][cc].x);
-        acc[cc][2] += g[u] * bf16_lo(w[u][cc].y);
-        acc[cc][3] += g[u] * bf16_hi(w[u][cc].y);
-        acc[cc][4] += g[u] * bf16_lo(w[u][cc].z);
-        acc[cc][5] += g[u] * bf16_hi(w[u][cc].z);
-        acc[cc][6] += g[u] * bf16_lo(w[u][cc].w);
-        acc[cc][7] += g[u] * bf16_hi(w[u][cc].w);
-      }
+        for (int cc = 0; cc < CPL; ++cc) {
+          acc[cc][0] += g[uu] * bf16_lo(w[uu][cc].x);
+          acc[cc][1] += g[uu] * bf16_hi(w[uu][cc].x);
+          acc[cc][2] += g[uu] * bf16_lo(w[uu][cc].y);
+          acc[cc][3] += g[uu] * bf16_hi(w[uu][cc].y);
+          acc[cc][4] += g[uu] * bf16_lo(w[uu][cc].z);
+          acc[cc][5] += g[uu] * bf16_hi(w[uu][cc].z);
+          acc[cc][6] += g[uu] * bf16_lo(w[uu][cc].w);
+          acc[cc][7] += g[uu] * bf16_hi(w[uu][cc].w);
+        }
+    }
   }
   if (!active) return;
   float* dst = part + ((int64_t)r * E + e) * dim;
