@@ -1,14 +1,24 @@
 // Exact top-k of each row of an fp32 score matrix, ordered (score desc, index asc).
 //
-// One 1024-thread workgroup per row:
-//   1. Radix select on order-preserving uint32 keys, 8 bits per pass from the most significant
-//      byte: an LDS histogram of the next digit among the elements that match the prefix found
-//      so far, then one wave scans the 256 bins from the top to find the bin holding the k-th
-//      largest key.  After four passes the k-th largest key K is known exactly, together with
-//      how many elements equal to K are needed (the rest of the k are strictly greater).
-//   2. Gather: every element with key > K is kept; among elements with key == K the lowest
-//      indices are kept, found with an in-order workgroup prefix count (ballot + popcount).
-//   3. A bitonic network in LDS sorts the k (key, index) pairs into (key desc, index asc).
+// One 1024-thread workgroup per row, keyed by the order-preserving uint32 map of the score and,
+// to break ties by lower index, the 64-bit key (score key << 32) | ~index (unique per row).
+//
+// Fast path (one pass over the row):
+//   1. Sample.  4096 scores from 64 evenly spaced runs of the row; the s-th largest sample key
+//      t (s chosen so that about 1.5 k + 12 n / 4096 row entries are expected at or above it)
+//      is found by a radix select in LDS.
+//   2. Stream.  Every entry with key >= t is appended to an LDS candidate list (kCap entries).
+//      If t is too high (fewer than k candidates) or the list overflows, the row takes the slow
+//      path.  Otherwise the candidates contain the top-k: any other entry is below t and at
+//      least k candidates are at or above it.
+//   3. Select.  The k-th largest 64-bit key K among the candidates (radix select, 8 passes of
+//      8 bits in LDS); the candidates with key >= K -- exactly k of them -- are sorted by a
+//      bitonic network and written out.
+// Rows of at most kCap entries are loaded whole and go straight to step 3.
+//
+// Slow path (any row, exact): the same radix select over the row in global memory, 4 passes on
+// the 32-bit key, then a gather of the entries above the k-th key and of the lowest-index
+// entries equal to it, and the same sort.
 #include "common.h"
 #include "kernels.h"
 
@@ -19,35 +29,34 @@ namespace {
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kMaxK = 1024;
+constexpr int kCap = 8192;      // LDS candidate list (keys and indices: 64 KiB)
+constexpr int kSamples = 4096;  // 64 runs of 64 consecutive entries
+constexpr int kUnroll = 8;      // loads in flight per thread while streaming
 
-__global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float* __restrict__ S,
-                                                             int64_t n, int64_t ld, int k,
-                                                             float* out_s, int64_t* out_i) {
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t sk[kMaxK];
-  __shared__ uint32_t si[kMaxK];
-  __shared__ uint32_t wave_cnt[kWaves];
-  __shared__ uint32_t sh_bin, sh_above, sh_gt;
+__device__ __forceinline__ unsigned long long key64(uint32_t key, uint32_t idx) {
+  return ((unsigned long long)key << 32) | (unsigned long long)(~idx);
+}
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const float* x = S + (int64_t)blockIdx.x * ld;
-
-  // ---- 1. radix select
-  uint32_t prefix = 0, pmask = 0;
-  uint32_t remaining = (uint32_t)k;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
+// Finds, among the `m` values produced by get(i), the `want`-th largest under the digits of
+// `bits`-bit keys (most significant digit first, 8 bits per pass).  Returns (prefix, needed):
+// the key itself and how many entries equal to it complete the count.
+template <int PASSES, class K, class Get>
+__device__ void radix_select(Get get, int64_t m, uint32_t want, uint32_t* hist, uint32_t* sh,
+                             K& out_key, uint32_t& out_need) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  K prefix = 0, pmask = 0;
+  uint32_t remaining = want;
+  for (int pass = 0; pass < PASSES; ++pass) {
+    const int shift = 8 * (PASSES - 1 - pass);
     if (tid < 256) hist[tid] = 0;
-    if (tid == 0) {  // defaults, only kept if the counts cannot reach k (precondition k <= n)
-      sh_bin = 0;
-      sh_above = 0;
+    if (tid == 0) {
+      sh[0] = 0;  // bin holding the wanted entry
+      sh[1] = 0;  // entries in higher bins
     }
     __syncthreads();
-    for (int64_t i = tid; i < n; i += kThreads) {
-      const uint32_t key = score_key(x[i]);
-      if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    for (int64_t i = tid; i < m; i += kThreads) {
+      const K key = get(i);
+      if ((key & pmask) == prefix) atomicAdd(&hist[(uint32_t)(key >> shift) & 255u], 1u);
     }
     __syncthreads();
     if (wave == 0) {
@@ -57,7 +66,7 @@ __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float* __rest
         c[j] = hist[255 - 4 * lane - j];
         tot += c[j];
       }
-      uint32_t incl = tot;  // count of keys in bins >= 252 - 4*lane (this lane's lowest bin)
+      uint32_t incl = tot;  // entries in bins >= 252 - 4 * lane
 #pragma unroll
       for (int o = 1; o < 64; o <<= 1) {
         const uint32_t y = __shfl_up(incl, o);
@@ -69,8 +78,8 @@ __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float* __rest
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           if (acc + c[j] >= remaining) {
-            sh_bin = 255u - 4u * lane - j;
-            sh_above = acc;
+            sh[0] = 255u - 4u * lane - j;
+            sh[1] = acc;
             break;
           }
           acc += c[j];
@@ -78,17 +87,136 @@ __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float* __rest
       }
     }
     __syncthreads();
-    prefix |= sh_bin << shift;
-    pmask |= 255u << shift;
-    remaining -= sh_above;
+    prefix |= (K)sh[0] << shift;
+    pmask |= (K)255u << shift;
+    remaining -= sh[1];
     __syncthreads();
   }
-  const uint32_t K = prefix;
-  const uint32_t need_eq = remaining;          // >= 1
-  const uint32_t n_gt = (uint32_t)k - need_eq;  // elements strictly above K
+  out_key = prefix;
+  out_need = remaining;
+}
 
-  // ---- 2. gather
-  if (tid == 0) sh_gt = 0;
+// Bitonic sort of P (a power of two, >= k) 64-bit keys in LDS, largest first; writes the first
+// k as (score, index) of row `row`.
+__device__ void sort_and_write(unsigned long long* sk, uint32_t k, int64_t row, float* out_s,
+                               int64_t* out_i) {
+  const int tid = threadIdx.x;
+  uint32_t P = 1;
+  while (P < k) P <<= 1;
+  for (uint32_t i = k + tid; i < P; i += kThreads) sk[i] = 0ull;  // below every real key
+  for (uint32_t size = 2; size <= P; size <<= 1) {
+    for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
+      __syncthreads();
+      for (uint32_t i = tid; i < P; i += kThreads) {
+        const uint32_t j = i ^ stride;
+        if (j > i) {
+          const bool desc = (i & size) == 0;
+          const unsigned long long a = sk[i], b = sk[j];
+          if ((b > a) == desc) {
+            sk[i] = b;
+            sk[j] = a;
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+  for (uint32_t p = tid; p < k; p += kThreads) {
+    out_s[row * k + p] = key_score((uint32_t)(sk[p] >> 32));
+    out_i[row * k + p] = (int64_t)(uint32_t)~(uint32_t)sk[p];
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float* __restrict__ S,
+                                                             int64_t n, int64_t ld, int k,
+                                                             float* out_s, int64_t* out_i) {
+  __shared__ uint32_t ckey[kCap];  // candidate keys (the sample first)
+  __shared__ uint32_t cidx[kCap];  // candidate indices
+  __shared__ unsigned long long sk[kMaxK];
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t sh[4];
+  __shared__ uint32_t wave_cnt[kWaves];
+  __shared__ uint32_t n_cand;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int64_t row = blockIdx.x;
+  const float* x = S + row * ld;
+
+  bool fast = true;
+  if (n <= kCap) {  // the whole row is the candidate list
+    for (int64_t i = tid; i < n; i += kThreads) {
+      ckey[i] = score_key(x[i]);
+      cidx[i] = (uint32_t)i;
+    }
+    if (tid == 0) n_cand = (uint32_t)n;
+    __syncthreads();
+  } else {
+    // 1. sample: run r covers entries [r * n / 64, + 64) -- n > kCap, so runs do not overlap
+    for (int s = tid; s < kSamples; s += kThreads) {
+      const int64_t i = (int64_t)(s >> 6) * n / 64 + (s & 63);
+      ckey[s] = score_key(x[i]);
+    }
+    const uint32_t want = (uint32_t)((3ll * k * kSamples + 2 * n - 1) / (2 * n)) + 12u;
+    uint32_t t;
+    uint32_t need;
+    radix_select<4, uint32_t>([&](int64_t i) { return ckey[i]; }, kSamples, want, hist, sh, t,
+                              need);
+    if (tid == 0) n_cand = 0;
+    __syncthreads();
+    // 2. stream the row once, appending the entries at or above t
+    for (int64_t base = 0; base < n; base += (int64_t)kThreads * kUnroll) {
+      float v[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int64_t i = base + (int64_t)u * kThreads + tid;
+        v[u] = i < n ? x[i] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int64_t i = base + (int64_t)u * kThreads + tid;
+        const uint32_t key = score_key(v[u]);
+        if (i < n && key >= t) {
+          const uint32_t p = atomicAdd(&n_cand, 1u);
+          if (p < kCap) {
+            ckey[p] = key;
+            cidx[p] = (uint32_t)i;
+          }
+        }
+      }
+    }
+    __syncthreads();
+    fast = n_cand >= (uint32_t)k && n_cand <= (uint32_t)kCap;  // uniform
+  }
+
+  if (fast) {
+    // 3. the k-th largest 64-bit key among the candidates; exactly k candidates reach it
+    const uint32_t m = n_cand;
+    unsigned long long K;
+    uint32_t need;
+    radix_select<8, unsigned long long>([&](int64_t i) { return key64(ckey[i], cidx[i]); }, m,
+                                        (uint32_t)k, hist, sh, K, need);
+    if (tid == 0) n_cand = 0;  // reused as the gather counter
+    __syncthreads();
+    for (uint32_t i = tid; i < m; i += kThreads) {
+      const unsigned long long key = key64(ckey[i], cidx[i]);
+      if (key >= K) {
+        const uint32_t p = atomicAdd(&n_cand, 1u);
+        if (p < (uint32_t)k) sk[p] = key;
+      }
+    }
+    sort_and_write(sk, (uint32_t)k, row, out_s, out_i);
+    return;
+  }
+
+  // ---- slow path: exact select over the row in global memory
+  uint32_t K;
+  uint32_t need_eq;
+  radix_select<4, uint32_t>([&](int64_t i) { return score_key(x[i]); }, n, (uint32_t)k, hist,
+                            sh, K, need_eq);
+  const uint32_t n_gt = (uint32_t)k - need_eq;  // entries strictly above K
+  if (tid == 0) n_cand = 0;
   __syncthreads();
   uint32_t eq_base = 0;
   for (int64_t base = 0; base < n; base += kThreads) {
@@ -101,17 +229,13 @@ __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float* __rest
       eq = key == K;
     }
     if (gt) {
-      const uint32_t p = atomicAdd(&sh_gt, 1u);
-      if (p < n_gt) {  // always true for finite inputs; keeps the stores in bounds regardless
-        sk[p] = key;
-        si[p] = (uint32_t)i;
-      }
+      const uint32_t p = atomicAdd(&n_cand, 1u);
+      if (p < n_gt) sk[p] = key64(key, (uint32_t)i);  // always true for finite inputs
     }
     const unsigned long long m = __ballot(eq);
     if (lane == 0) wave_cnt[wave] = (uint32_t)__popcll(m);
     __syncthreads();
-    const uint32_t gt_found = sh_gt;  // stable here: this chunk's atomics are done, the next
-                                      // chunk's start after the barrier below
+    const uint32_t gt_found = n_cand;  // stable: this chunk's atomics are done
     uint32_t before = 0, chunk_total = 0;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
@@ -119,56 +243,22 @@ __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float* __rest
       before += w < wave ? cw : 0u;
       chunk_total += cw;
     }
-    if (eq) {
+    if (eq) {  // the lowest-index entries equal to K, in index order
       const uint32_t r = eq_base + before + (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
-      if (r < need_eq) {
-        sk[n_gt + r] = key;
-        si[n_gt + r] = (uint32_t)i;
-      }
+      if (r < need_eq) sk[n_gt + r] = key64(key, (uint32_t)i);
     }
     eq_base += chunk_total;
     __syncthreads();
     if (eq_base >= need_eq && gt_found == n_gt) break;  // everything needed is collected
   }
-
-  // ---- 3. sort the k pairs: (key desc, index asc)
-  uint32_t P = 1;
-  while (P < (uint32_t)k) P <<= 1;
-  for (uint32_t i = k + tid; i < P; i += kThreads) {
-    sk[i] = 0u;  // below every finite score's key
-    si[i] = 0xffffffffu;
-  }
-  for (uint32_t size = 2; size <= P; size <<= 1) {
-    for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
-      __syncthreads();
-      for (uint32_t i = tid; i < P; i += kThreads) {
-        const uint32_t j = i ^ stride;
-        if (j > i) {
-          const bool up = (i & size) == 0;
-          const uint32_t ki = sk[i], kj = sk[j], ii = si[i], ij = si[j];
-          const bool j_first = kj > ki || (kj == ki && ij < ii);
-          if (j_first == up) {
-            sk[i] = kj;
-            sk[j] = ki;
-            si[i] = ij;
-            si[j] = ii;
-          }
-        }
-      }
-    }
-  }
-  __syncthreads();
-  for (int p = tid; p < k; p += kThreads) {
-    out_s[(int64_t)blockIdx.x * k + p] = key_score(sk[p]);
-    out_i[(int64_t)blockIdx.x * k + p] = (int64_t)si[p];
-  }
+  sort_and_write(sk, (uint32_t)k, row, out_s, out_i);
 }
 
 }  // namespace
 
 hipError_t launch_topk_rows(const float* scores, int64_t rows, int64_t n, int64_t ld, int k,
                             float* out_scores, int64_t* out_idx, hipStream_t stream) {
-  if (k < 1 || k > kMaxK || rows < 1) return hipErrorInvalidValue;
+  if (k < 1 || k > kMaxK || rows < 1 || n >= (int64_t(1) << 32) - 1) return hipErrorInvalidValue;
   hipLaunchKernelGGL(topk_rows_kernel, dim3((unsigned)rows), dim3(kThreads), 0, stream, scores,
                      n, ld, k, out_scores, out_idx);
   return hipGetLastError();

@@ -180,6 +180,57 @@ def test_topk_all_equal_scores_returns_lowest_indices():
     assert torch.all(s[0] == s[0, 0])
 
 
+
+@pytest.mark.parametrize("n_docs,k", [(9000, 10), (20000, 100), (40000, 1000)])
+def test_topk_streaming_select_long_rows(n_docs, k):
+    # rows longer than the LDS candidate list: sampled threshold, one streaming pass
+    g = torch.Generator().manual_seed(n_docs + k)
+    lens = torch.randint(1, 6, (n_docs,), generator=g)
+    Q, D, off = _ragged(n_docs + k, 3, 4, lens.tolist(), 32)
+    s, i = hpr.maxsim_topk(*_to_dev(Q, D, off), k)
+    O = oracle.maxsim_scores(_bf(Q), _bf(D), off.numpy())
+    s, i = s.cpu().numpy(), i.cpu().numpy()
+    for q in range(3):
+        check_topk(s[q], i[q], O[q], k)
+
+
+def test_topk_long_row_of_equal_scores_takes_exact_path():
+    # every entry ties with the sampled threshold, so the candidate list overflows and the row
+    # is selected by the exact multi-pass path: the lowest indices win
+    Q, D, off = _ragged(33, 1, 4, [3], 32)
+    n = 20000
+    D2 = torch.cat([D] * n)
+    off2 = synth.csr_offsets(torch.full((n,), 3))
+    s, i = hpr.maxsim_topk(*_to_dev(Q, D2, off2), 1000)
+    assert i[0].tolist() == list(range(1000))
+    assert torch.all(s[0] == s[0, 0])
+
+
+def test_topk_unrepresentative_sample_takes_exact_path():
+    # the documents the sampler reads (64 runs of 64 at r * n / 64) score highest and are the
+    # only high ones: the threshold then admits fewer than k candidates and the exact path runs
+    n, k = 10000, 200
+    sampled = set()
+    for sidx in range(4096):
+        sampled.add((sidx >> 6) * n // 64 + (sidx & 63))
+    g = torch.Generator().manual_seed(5)
+    Q = synth.unit_rows(4, 32, g, "cpu", torch.bfloat16).reshape(1, 4, 32)
+    low = synth.unit_rows(n, 32, g, "cpu", torch.bfloat16)
+    noise = synth.unit_rows(n * 4, 32, g, "cpu", torch.float32).reshape(n, 4, 32)
+    docs = []
+    for d in range(n):
+        if d in sampled:  # the query's tokens, perturbed per document: distinct high scores
+            docs.append(synth._normalise(Q[0].float() + 0.3 * noise[d]).to(torch.bfloat16))
+        else:
+            docs.append(low[d:d + 1])
+    lens = torch.tensor([t.shape[0] for t in docs])
+    D = torch.cat(docs)
+    off = synth.csr_offsets(lens)
+    s, i = hpr.maxsim_topk(*_to_dev(Q, D, off), k)
+    O = oracle.maxsim_scores(_bf(Q), _bf(D), off.numpy())
+    r = check_topk(s.cpu().numpy()[0], i.cpu().numpy()[0], O[0], k)
+    assert set(i.cpu().numpy()[0].tolist()) <= sampled
+
 # ------------------------------------------------------------------------------ InfoNCE loss
 
 def _loss_parity(Q, D, off, pos, scale, rel_grad=REL):
