@@ -62,7 +62,7 @@ typedef int32_t hpr_status;
 #define HPR_ABI_VERSION 1
 
 /* Shape limits of this build (HPR_ERR_UNSUPPORTED_SHAPE beyond them).
- *   MaxSim calls: dim % 8 == 0, 8 <= dim <= 256; lq <= 128 when dim <= 64, lq <= 64 when
+ *   MaxSim calls: dim % 8 == 0, 8 <= dim <= 256; lq <= 128 when dim <= 128, lq <= 64 when
  *     dim <= 256; coltrast_loss_fwd_bwd: lq <= 64 when dim <= 128, lq <= 32 when dim <= 256;
  *     n_tok < 2^31 (a store of 2^31 bf16 tokens of dim 128 would not fit one GPU's HBM).
  *   Top-k: 1 <= k <= min(n, 1024) (k outside that range is HPR_ERR_INVALID_ARG).

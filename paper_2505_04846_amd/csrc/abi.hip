@@ -103,7 +103,7 @@ hpr_status check_maxsim_args(const uint16_t* q, int32_t nq, int32_t lq, const ui
 // Query-length limit of the MaxSim kernels (query slots a wave holds).
 hpr_status check_lq(int32_t lq, int32_t dim, bool argmax) {
   const int lqp = (lq + 31) / 32 * 32;
-  const int max_slots = argmax ? (dim <= 128 ? 64 : 32) : (dim <= 64 ? 128 : 64);
+  const int max_slots = argmax ? (dim <= 128 ? 64 : 32) : (dim <= 128 ? 128 : 64);
   if (lqp > max_slots)
     return fail(HPR_ERR_UNSUPPORTED_SHAPE, "lq=%d exceeds the limit %d for dim=%d%s", lq,
                 max_slots, dim, argmax ? " in the loss" : "");

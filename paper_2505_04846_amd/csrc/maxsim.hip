@@ -106,10 +106,12 @@ __device__ __forceinline__ float half32_sum(float v) {
   return v;
 }
 
-// Waves per SIMD the register allocation must allow: three for the plain dim-128 variant
-// (168 VGPRs), two otherwise.
+// Waves per SIMD the register allocation must allow: two (up to 256 VGPRs), which leaves the
+// dim-128 plain variant room for 128 query slots per wave (measured 7-10 % faster than 64
+// slots at three waves per SIMD: half the LDS operand reads per MFMA and half the query groups,
+// hence half the document-range re-reads).
 template <int KS, bool ARGMAX>
-constexpr int maxsim_occupancy() { return (!ARGMAX && KS == 8) ? 3 : 2; }
+constexpr int maxsim_occupancy() { return 2; }
 
 template <int KS, int NB, int WPW, bool ARGMAX>
 __global__ __launch_bounds__(64 * WPW, (maxsim_occupancy<KS, ARGMAX>())) void maxsim_kernel(
@@ -438,9 +440,9 @@ hipError_t launch_t(const MaxsimPlan& plan, const MaxsimArgs& args, hipStream_t 
   return hipGetLastError();
 }
 
-// Variants by k-steps of 16 (dim <= 16 KS).  Query slots per wave: 128 (plain, dim <= 64),
-// 64 (plain, dim 128 and 256; argmax, dim <= 128), 32 (argmax, dim 256) -- what fits two
-// waves per SIMD in 256 registers next to the argmax variants' 18 state registers per block.
+// Variants by k-steps of 16 (dim <= 16 KS).  Query slots per wave: 128 (plain, dim <= 128),
+// 64 (plain, dim 256; argmax, dim <= 128), 32 (argmax, dim 256) -- what fits two waves per
+// SIMD in 256 registers next to the argmax variants' 18 state registers per block.
 hipError_t launch_variant(const MaxsimPlan& plan, const MaxsimArgs& args, bool argmax,
                           hipStream_t stream) {
   if (argmax) {
@@ -455,7 +457,7 @@ hipError_t launch_variant(const MaxsimPlan& plan, const MaxsimArgs& args, bool a
   switch (plan.ks) {
     case 2: return launch_t<2, 4, 4, false>(plan, args, stream);
     case 4: return launch_t<4, 4, 4, false>(plan, args, stream);
-    case 8: return launch_t<8, 2, 4, false>(plan, args, stream);
+    case 8: return launch_t<8, 4, 4, false>(plan, args, stream);
     case 16: return launch_t<16, 2, 4, false>(plan, args, stream);
     default: return hipErrorInvalidValue;
   }
@@ -467,17 +469,20 @@ bool maxsim_plan(int nq, int lq, int64_t n_docs, int64_t n_tok, int dim, bool ar
                  MaxsimPlan* p) {
   if (dim < 8 || dim > 256 || dim % 8 != 0 || lq < 1 || nq < 1 || n_docs < 1) return false;
   p->ks = dim <= 32 ? 2 : dim <= 64 ? 4 : dim <= 128 ? 8 : 16;
-  p->nb = argmax ? (p->ks == 16 ? 1 : 2) : (p->ks >= 8 ? 2 : 4);
+  p->nb = argmax ? (p->ks == 16 ? 1 : 2) : (p->ks == 16 ? 2 : 4);
   p->wpw = 4;
   p->lqp = (lq + 31) / 32 * 32;
   if (p->lqp > p->nb * 32) return false;
   p->qpw = p->nb * 32 / p->lqp;
   const int64_t q_per_wg = (int64_t)p->qpw * p->wpw;
   p->n_qgroups = (int)((nq + q_per_wg - 1) / q_per_wg);
-  // Enough workgroups to fill every CU's resident slots four times over, but no range shorter
-  // than ~1024 tokens (the query operands are re-loaded by every workgroup).
-  const int occ = (!argmax && p->ks == 8) ? 3 : 2;  // resident workgroups per CU
-  const int64_t target_wg = (int64_t)(n_cu > 0 ? n_cu : 256) * occ * 4;
+  // Workgroups: the plain score takes enough to fill every CU's two resident slots eight times
+  // over (short ranges keep the workgroups sharing a range in step, so the range is served from
+  // L2); the argmax variant, whose stores are short, takes one round of resident workgroups
+  // (fewer per-workgroup prologues).  No range is shorter than ~1024 tokens (the query operands
+  // are re-loaded by every workgroup).
+  const int occ = 2;  // resident workgroups per CU
+  const int64_t target_wg = (int64_t)(n_cu > 0 ? n_cu : 256) * occ * (argmax ? 1 : 8);
   int64_t R = (target_wg + p->n_qgroups - 1) / p->n_qgroups;
   const int64_t max_by_tokens = n_tok / 1024 > 0 ? n_tok / 1024 : 1;
   if (R > max_by_tokens) R = max_by_tokens;

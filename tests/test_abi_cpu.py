@@ -56,7 +56,7 @@ def _score(**kw):
     (dict(q=NULL), 1), (dict(d=NULL), 1), (dict(off=NULL), 1), (dict(scores=NULL), 1),
     (dict(ws=NULL), 1), (dict(nq=0), 1), (dict(lq=0), 1), (dict(n_docs=0), 1),
     (dict(n_tok=3), 1), (dict(dim=0), 1), (dict(dim=12), 4), (dict(dim=264), 4), (dict(dim=4), 4),
-    (dict(lq=129, dim=64), 4), (dict(lq=65), 4), (dict(lq=65, dim=256), 4), (dict(q=FAKE_ODD), 1), (dict(ws_bytes=0), 5),
+    (dict(lq=129, dim=64), 4), (dict(lq=129), 4), (dict(lq=65, dim=256), 4), (dict(q=FAKE_ODD), 1), (dict(ws_bytes=0), 5),
 ])
 def test_maxsim_score_rejects(kw, status):
     assert _score(**kw) == status

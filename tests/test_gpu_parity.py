@@ -81,6 +81,9 @@ def test_tiny_maxsim_scores_match_oracle():
     (9, 32, [513, 7, 64, 200], 128),
     (4, 100, [40, 41], 64),
     (3, 64, [20, 260, 3], 128),
+    (3, 100, [40, 300, 7], 128),
+    (2, 128, [70, 33, 1], 128),
+    (5, 96, [64, 65], 120),
     (2, 128, [9, 70], 48),
     (6, 64, [33, 1, 90], 256),
     (2, 33, [50, 17], 192),
