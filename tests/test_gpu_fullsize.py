@@ -1,0 +1,166 @@
+"""GPU parity at the full workload sizes, in the launch configuration the benchmark times.
+
+The workloads are generated exactly as the benchmark generates them (same seeds and shapes) and
+the same entry point is called with the same arguments.  The fp64 CPU oracle cannot score these
+stores in full, so:
+
+  * every query's list is checked for structure (indices in range and distinct, sorted by
+    (score desc, index asc));
+  * a seeded sample of returned (query, index, score) entries is checked against the oracle's
+    score of that (query, document), computed one by one (tolerance 2e-3 and the tight 1e-4 for
+    MaxSim, whose bf16 products are exact in fp32);
+  * for a few queries the exact top-k set is checked against the oracle over a candidate set
+    screened in float64 by plain torch (tests/screen.py), with the screening margin asserted, at
+    the 2e-3 tolerance and again at a tight one (1e-5 for MaxSim, 1e-4 for the dense store);
+  * the dense store's 1,000 planted near-duplicates must each rank first for their query.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2505_04846_amd as hpr
+import synth
+from screen import SCREEN_ABS_ERR, candidates, dense_row_f64, maxsim_row_f64, virtual_row
+from topk_check import check_topk, tol
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+REL = 2e-3
+
+
+def _bf(t):
+    return oracle.decode_bf16(t.detach().cpu().contiguous().view(torch.int16).numpy())
+
+
+def _f16(t):
+    return oracle.decode_fp16(t.detach().cpu().contiguous().view(torch.int16).numpy())
+
+
+def _doc_tokens(D, off, docs):
+    """Tokens of the given documents (in the given order), gathered on the GPU, with CSR offsets
+    rebased to the gathered block."""
+    docs = torch.as_tensor(np.asarray(docs), dtype=torch.int64, device=D.device)
+    lo, hi = off[docs], off[docs + 1]
+    lens = hi - lo
+    starts = torch.repeat_interleave(lo - (torch.cumsum(lens, 0) - lens), lens)
+    rows = torch.arange(int(lens.sum()), device=D.device) + starts
+    sub_off = torch.zeros(docs.numel() + 1, dtype=torch.int64)
+    sub_off[1:] = torch.cumsum(lens.cpu(), 0)
+    return _bf(D[rows]), sub_off.numpy()
+
+
+def _oracle_maxsim(Qq_h, D, off, docs):
+    Dh, sub_off = _doc_tokens(D, off, docs)
+    return oracle.maxsim_scores(Qq_h[None], Dh, sub_off)[0]
+
+
+def _check_structure(s, i, n):
+    assert np.all((i >= 0) & (i < n)), "index out of range"
+    nq, k = i.shape
+    srt = np.sort(i, axis=1)
+    assert np.all(srt[:, 1:] != srt[:, :-1]), "duplicate index in a list"
+    a, b = s[:, :-1], s[:, 1:]
+    ok = (a > b) | ((a == b) & (i[:, :-1] < i[:, 1:]))
+    assert ok.all(), f"unsorted lists: {np.nonzero(~ok.all(axis=1))[0][:5]}"
+
+
+def _maxsim_fullsize(w, n_samples, queries, m_screen):
+    Q, D, off, k = w["Q"], w["D"], w["off"], w["k"]
+    nq, n_docs = Q.shape[0], off.numel() - 1
+    ws = torch.empty(hpr.lib().maxsim_topk_workspace_size(nq, Q.shape[1], n_docs, D.shape[0],
+                                                          D.shape[1], k),
+                     dtype=torch.uint8, device=DEV)
+    s, i = hpr.maxsim_topk(Q, D, off, k, ws=ws)  # the benchmark's call
+    del ws
+    s, i = s.cpu().numpy(), i.cpu().numpy()
+    _check_structure(s, i, n_docs)
+    Qh = _bf(Q)
+    rng = np.random.default_rng(0)
+    # sampled returned entries, one by one
+    pick_q = rng.integers(0, nq, n_samples)
+    pick_r = rng.integers(0, k, n_samples)
+    got, want = [], []
+    for q, r in zip(pick_q, pick_r):
+        got.append(s[q, r])
+        want.append(_oracle_maxsim(Qh[q], D, off, [i[q, r]])[0])
+    got, want = np.array(got), np.array(want)
+    err = np.abs(got - want)
+    assert np.all(err <= REL * np.maximum(np.abs(want), 1e-3)), "sampled score outside 2e-3"
+    assert np.all(err <= 1e-4 * np.maximum(np.abs(want), 1e-3)), "sampled score outside 1e-4"
+    # exact top-k sets of a few queries over float64-screened candidates
+    exact = 0
+    for q in queries:
+        row = maxsim_row_f64(Q[q], D, off)
+        cand, outside = candidates(row, i[q], m_screen)
+        del row
+        o = _oracle_maxsim(Qh[q], D, off, cand)
+        t_c = np.sort(o)[::-1][k - 1]
+        assert outside + SCREEN_ABS_ERR < t_c - tol(t_c, REL), \
+            f"query {q}: screening margin too small ({outside} vs {t_c})"
+        full = virtual_row(n_docs, cand, o, floor=min(o.min(), outside) - 1.0)
+        res = check_topk(s[q], i[q], full, k, rel=REL)
+        # the tight pass: bf16 products are exact in fp32, so the GPU differs from the oracle
+        # only by fp32 summation (~1e-6 relative); any index, sign or operand mistake fails it
+        check_topk(s[q], i[q], full, k, rel=1e-5)
+        exact += res["exact"]
+        print(f"query {q}: {cand.size} candidates, best outside {outside:.6f}, oracle k-th "
+              f"{t_c:.6f}, exact order {res['exact']}, tolerance exception {res['exception_used']}")
+    return exact
+
+
+def test_li_retrieval_fullsize():
+    # 1,024 x 32 queries vs 500,000 documents (Ld uniform in [32, 384]), dim 128, top-100
+    w = synth.li_retrieval(seed=0, device=DEV)
+    _maxsim_fullsize(w, n_samples=400, queries=[0, 1, 517, 1023], m_screen=1000)
+    del w
+    torch.cuda.empty_cache()
+
+
+def test_li_large_fullsize():
+    # 4,096 x 64 queries vs 1,000,000 lognormal documents with 10 % noisy clones, top-1000
+    w = synth.li_large(seed=0, device=DEV)
+    _maxsim_fullsize(w, n_samples=300, queries=[0, 2049, 4095], m_screen=3000)
+    del w
+    torch.cuda.empty_cache()
+
+
+def test_dense_retrieval_fullsize():
+    # 4,096 queries vs 10,000,000 fp16 rows of dim 4096, 1,000 planted rows, top-100
+    w = synth.dense_retrieval(seed=0, device=DEV)
+    Q, X, k = w["Q"], w["X"], w["k"]
+    nq, n = Q.shape[0], X.shape[0]
+    ws = hpr.dense_workspace(Q, X, k)
+    s, i = hpr.dense_ip_topk(Q, X, k, ws=ws)  # the benchmark's call
+    del ws
+    s, i = s.cpu().numpy(), i.cpu().numpy()
+    _check_structure(s, i, n)
+    pq, pr = w["planted_q"].cpu().numpy(), w["planted_row"].cpu().numpy()
+    assert np.array_equal(i[pq, 0], pr), "a planted row is not its query's first result"
+    Qh = _f16(Q)
+    o = np.sum(Qh[pq] * _f16(X[torch.as_tensor(pr, device=DEV)]), axis=1)
+    assert np.all(np.abs(s[pq, 0] - o) <= REL * np.abs(o))
+    rng = np.random.default_rng(0)
+    pick_q = rng.integers(0, nq, 300)
+    pick_r = rng.integers(0, k, 300)
+    rows = torch.as_tensor(i[pick_q, pick_r], device=DEV)
+    want = np.sum(Qh[pick_q] * _f16(X[rows]), axis=1)
+    got = s[pick_q, pick_r]
+    assert np.all(np.abs(got - want) <= REL * np.maximum(np.abs(want), 1e-3))
+    unplanted = sorted(set(range(nq)) - set(pq.tolist()))
+    for q in [int(pq[0]), int(pq[-1]), unplanted[0], unplanted[-1]]:
+        row = dense_row_f64(Q[q], X)
+        cand, outside = candidates(row, i[q], 1000)
+        del row
+        oc = oracle.dense_scores(Qh[q][None], _f16(X[torch.as_tensor(cand, device=DEV)]))[0]
+        t_c = np.sort(oc)[::-1][k - 1]
+        assert outside + SCREEN_ABS_ERR < t_c - tol(t_c, REL), f"query {q}: screening margin"
+        full = virtual_row(n, cand, oc, floor=min(oc.min(), outside) - 1.0)
+        res = check_topk(s[q], i[q], full, k, rel=REL)
+        check_topk(s[q], i[q], full, k, rel=1e-4)  # fp32 sums of 4096 exact products
+        print(f"query {q}: {cand.size} candidates, best outside {outside:.6f}, oracle k-th "
+              f"{t_c:.6f}, exact order {res['exact']}, tolerance exception {res['exception_used']}")
+    del w, Q, X
+    torch.cuda.empty_cache()
