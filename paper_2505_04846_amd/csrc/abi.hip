@@ -110,6 +110,10 @@ hpr_status check_lq(int32_t lq, int32_t dim, bool argmax) {
   return HPR_OK;
 }
 
+// Control words of the loss call: the error flag and the InfoNCE completion counter (both
+// zeroed by the partition kernel of the call).
+constexpr int kLossCtrlWords = 2;
+
 size_t part_bytes(int64_t n_docs) {
   const int64_t r = n_docs < kMaxRanges ? n_docs : kMaxRanges;
   return align_up((size_t)(r + 1) * sizeof(int64_t));
@@ -130,7 +134,7 @@ struct Carver {
 
 hpr_status run_maxsim(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d_tok,
                       const int64_t* d_off, int64_t n_docs, int64_t n_tok, int32_t dim,
-                      float* scores, uint16_t* amax, int32_t* flag, int64_t* part,
+                      float* scores, uint16_t* amax, int32_t* ctrl, int n_ctrl, int64_t* part,
                       hipStream_t stream) {
   int n_cu = 0;
   hpr_status st = current_cu_count(&n_cu);
@@ -139,12 +143,12 @@ hpr_status run_maxsim(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t*
   if (!maxsim_plan(nq, lq, n_docs, n_tok, dim, amax != nullptr, n_cu, &plan))
     return fail(HPR_ERR_UNSUPPORTED_SHAPE, "no MaxSim plan for this shape");
   hipError_t e = timed("partition", stream, [&] {
-    return launch_partition(d_off, n_docs, n_tok, plan.n_ranges, part, flag, stream);
+    return launch_partition(d_off, n_docs, n_tok, plan.n_ranges, part, ctrl, n_ctrl, stream);
   });
   if (e != hipSuccess) return hip_fail(e, "partition launch");
   e = timed(amax ? "maxsim_argmax" : "maxsim", stream, [&] {
     return launch_maxsim(plan, q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, part, scores, amax,
-                         flag, stream);
+                         ctrl, stream);
   });
   if (e != hipSuccess) return hip_fail(e, "maxsim launch");
   return HPR_OK;
@@ -176,7 +180,7 @@ size_t coltrast_loss_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int6
   const int64_t E = (int64_t)nq * lq;
   const size_t gq = align_up((size_t)grad_q_ranges(n_docs, n_tok, E, dim) * (size_t)E *
                              (size_t)dim * sizeof(float));
-  return 2 * sd + am + part_bytes(n_docs) + align_up(2 * sizeof(int32_t)) +
+  return 2 * sd + am + part_bytes(n_docs) + align_up((size_t)kLossCtrlWords * sizeof(int32_t)) +
          align_up((size_t)nq * sizeof(float)) + gq;
 }
 
@@ -192,8 +196,8 @@ hpr_status maxsim_score(const uint16_t* q, int32_t nq, int32_t lq, const uint16_
     return fail(HPR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu < %zu bytes", ws_bytes, need);
   Carver c(ws);
   int64_t* part = c.take<int64_t>(part_bytes(n_docs));
-  return run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, scores, nullptr, nullptr, part,
-                    static_cast<hipStream_t>(stream));
+  return run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, scores, nullptr, nullptr, 0,
+                    part, static_cast<hipStream_t>(stream));
 }
 
 hpr_status maxsim_topk(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d_tok,
@@ -214,7 +218,8 @@ hpr_status maxsim_topk(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t
   Carver c(ws);
   float* scores = c.take<float>((size_t)nq * n_docs * sizeof(float));
   int64_t* part = c.take<int64_t>(part_bytes(n_docs));
-  st = run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, scores, nullptr, nullptr, part, s);
+  st = run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, scores, nullptr, nullptr, 0, part,
+                  s);
   if (st != HPR_OK) return st;
   hipError_t e = timed("topk", s, [&] {
     return launch_topk_rows(scores, nq, n_docs, n_docs, k, out_scores, out_idx, s);
@@ -247,25 +252,31 @@ hpr_status coltrast_loss_fwd_bwd(const uint16_t* q, int32_t nq, int32_t lq,
   float* G = c.take<float>((size_t)nq * n_docs * sizeof(float));
   uint16_t* amax = c.take<uint16_t>((size_t)n_docs * nq * lq * sizeof(uint16_t));
   int64_t* part = c.take<int64_t>(part_bytes(n_docs));
-  int32_t* ctrl = c.take<int32_t>(2 * sizeof(int32_t));
+  const int n_ctrl = kLossCtrlWords;
+  int32_t* ctrl = c.take<int32_t>((size_t)n_ctrl * sizeof(int32_t));
   float* terms = c.take<float>((size_t)nq * sizeof(float));
   float* gq_part = c.take<float>((size_t)grad_q_ranges(n_docs, n_tok, (int64_t)nq * lq, dim) *
                                  (size_t)nq * lq * dim * sizeof(float));
-  st = run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, S, amax, ctrl, part, s);
+  st = run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, S, amax, ctrl, n_ctrl, part, s);
   if (st != HPR_OK) return st;
   hipError_t e = timed("infonce", s, [&] {
     return launch_infonce(S, nq, n_docs, pos_idx, logit_scale, G, terms, loss, scores, ctrl, s);
   });
   if (e != hipSuccess) return hip_fail(e, "infonce launch");
+  // With both gradients, the last step of dQ (the sum over its document ranges) rides in the
+  // dD launch, saving a kernel launch.
+  const bool fold = dq && dd;
   if (dq) {
     e = timed("grad_q", s, [&] {
-      return launch_grad_q(d_tok, d_off, n_docs, n_tok, dim, nq, lq, amax, G, gq_part, dq, s);
+      return launch_grad_q(d_tok, d_off, n_docs, n_tok, dim, nq, lq, amax, G, gq_part, dq, fold,
+                           s);
     });
     if (e != hipSuccess) return hip_fail(e, "dQ launch");
   }
   if (dd) {
     e = timed("grad_d", s, [&] {
-      return launch_grad_d(q, d_off, n_docs, n_tok, dim, nq, lq, amax, G, dd, s);
+      return launch_grad_d(q, d_off, n_docs, n_tok, dim, nq, lq, amax, G, dd,
+                           fold ? gq_part : nullptr, dq, s);
     });
     if (e != hipSuccess) return hip_fail(e, "dD launch");
   }

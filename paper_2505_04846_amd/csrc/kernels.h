@@ -29,10 +29,10 @@ bool maxsim_plan(int nq, int lq, int64_t n_docs, int64_t n_tok, int dim, bool ar
                  MaxsimPlan* plan);
 
 // part[r], r = 0..R: first document of range r (token-balanced, documents never split).
-// Also zeroes ctrl[0] and ctrl[1] (if ctrl is non-null): the error flag and the completion
-// counter used by later kernels of the same call.
+// Also zeroes ctrl[0 .. n_ctrl) (if ctrl is non-null): the error flag and the completion
+// counters used by later kernels of the same call.
 hipError_t launch_partition(const int64_t* off, int64_t n_docs, int64_t n_tok, int n_ranges,
-                            int64_t* part, int32_t* ctrl, hipStream_t stream);
+                            int64_t* part, int32_t* ctrl, int n_ctrl, hipStream_t stream);
 
 // MaxSim scores (and, when amax != nullptr, the lowest-index argmax token per (q, i, d), stored
 // as uint16 [n_docs, nq * lq]; a document longer than 65536 tokens raises *flag).
@@ -58,16 +58,18 @@ hipError_t launch_infonce(const float* S, int nq, int64_t n_docs, const int32_t*
                           float scale, float* G, float* terms, float* loss, float* scores_out,
                           int32_t* ctrl, hipStream_t stream);
 
-// dQ in two passes over `grad_q_ranges` document ranges; part holds
-// grad_q_ranges(...) * nq * lq * dim floats of partial sums.
+// dQ over `grad_q_ranges` document ranges; part holds grad_q_ranges(...) * nq * lq * dim
+// floats of partial sums.  With defer_sum the sum over the ranges is left to launch_grad_d
+// (which must then be given part and dq).
 int grad_q_ranges(int64_t n_docs, int64_t n_tok, int64_t E, int dim);
 hipError_t launch_grad_q(const uint16_t* d_tok, const int64_t* off, int64_t n_docs, int64_t n_tok,
                          int dim, int nq, int lq, const uint16_t* amax, const float* G,
-                         float* part, float* dq, hipStream_t stream);
+                         float* part, float* dq, bool defer_sum, hipStream_t stream);
 
+// dD; when dq_part is non-null it also finishes a deferred dQ (sums dq_part's ranges into dq).
 hipError_t launch_grad_d(const uint16_t* q, const int64_t* off, int64_t n_docs, int64_t n_tok,
                          int dim, int nq, int lq, const uint16_t* amax, const float* G, float* dd,
-                         hipStream_t stream);
+                         const float* dq_part, float* dq, hipStream_t stream);
 
 hipError_t launch_scale(float* x, int64_t n, const float* scale, hipStream_t stream);
 

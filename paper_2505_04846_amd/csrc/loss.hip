@@ -148,7 +148,8 @@ template <int CPL>
 __global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
     const uint16_t* __restrict__ D, const int64_t* __restrict__ off, int64_t n_docs,
     int64_t n_tok, int dim, int nq, int lq, const uint16_t* __restrict__ amax,
-    const float* __restrict__ G, float* __restrict__ part, int n_groups, int R) {
+    const float* __restrict__ G, float* __restrict__ part, float* __restrict__ dq, int n_groups,
+    int R) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t lin = xcd_linear(blockIdx.x, (int64_t)n_groups * R);
   const int r = (int)(lin / n_groups);
@@ -221,7 +222,7 @@ __global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
     }
   }
   if (!active) return;
-  float* dst = part + ((int64_t)r * E + e) * dim;
+  float* dst = (R == 1 ? dq : part + (int64_t)r * E * dim) + e * dim;  // one range: final sums
 #pragma unroll
   for (int cc = 0; cc < CPL; ++cc) {
     const int k = 8 * (c + 16 * cc);
@@ -232,15 +233,33 @@ __global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
   }
 }
 
-// dQ, second pass: dq[i] = sum over ranges r = 0, 1, ... of part[r][i] (4 values per thread).
+// dQ, second pass: dq[i] = sum over ranges r = 0, 1, ... of part[r][i], 4 values at a time.
+// Run by its own kernel, or folded into the first lines of grad_d_kernel (the next launch of the
+// call), whose workgroups each take one slice of the values.
+__device__ __forceinline__ void grad_q_sum_ranges(const float* __restrict__ part, int R,
+                                                  int64_t i0, int64_t i1, int64_t n4,
+                                                  float* __restrict__ dq) {
+  const f32x4* p = reinterpret_cast<const f32x4*>(part);
+  for (int64_t i = i0 + threadIdx.x; i < i1; i += blockDim.x) {
+    f32x4 s = p[i];
+    int r = 1;
+    for (; r + 8 <= R; r += 8) {  // eight ranges' loads in flight, then added in range order
+      f32x4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = p[(int64_t)(r + u) * n4 + i];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; r < R; ++r) s += p[(int64_t)r * n4 + i];
+    reinterpret_cast<f32x4*>(dq)[i] = s;
+  }
+}
+
 __global__ void grad_q_reduce_kernel(const float* __restrict__ part, int R, int64_t n4,
                                      float* __restrict__ dq) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n4) return;
-  const f32x4* p = reinterpret_cast<const f32x4*>(part);
-  f32x4 s = p[i];
-  for (int r = 1; r < R; ++r) s += p[(int64_t)r * n4 + i];
-  reinterpret_cast<f32x4*>(dq)[i] = s;
+  const int64_t i0 = (int64_t)blockIdx.x * blockDim.x;
+  const int64_t i1 = i0 + blockDim.x < n4 ? i0 + blockDim.x : n4;
+  grad_q_sum_ranges(part, R, i0, i1, n4, dq);
 }
 
 constexpr int kGdWaves = 16;
@@ -257,8 +276,7 @@ __host__ __device__ inline int gd_tpr(int dim) { return dim <= 64 ? 2 : dim <= 1
 struct GdLds {
   int keys, sorted, cnt, rs, gcol, total;
 };
-__host__ __device__ inline GdLds gd_lds(int E, int nq, int dim) {
-  const int rpp = kGdThreads / gd_tpr(dim);
+__host__ __device__ inline GdLds gd_lds(int E, int nq, int rpp) {
   GdLds l;
   l.keys = 0;  // the document's argmax entries, staged once
   l.sorted = (2 * E + 15) / 16 * 16;
@@ -284,11 +302,18 @@ template <int TPR>
 __global__ __launch_bounds__(kGdThreads) void grad_d_kernel(
     const uint16_t* __restrict__ Q, const int64_t* __restrict__ off, int64_t n_docs,
     int64_t n_tok, int dim, int nq, int lq, uint64_t lq_magic,
-    const uint16_t* __restrict__ amax, const float* __restrict__ G, float* __restrict__ dd) {
+    const uint16_t* __restrict__ amax, const float* __restrict__ G, float* __restrict__ dd,
+    const float* __restrict__ dq_part, int dq_R, float* __restrict__ dq) {
   extern __shared__ __attribute__((aligned(16))) unsigned char gd_smem[];
   constexpr int RPP = kGdThreads / TPR;
+  if (dq_part) {  // the dQ range sums, one slice per workgroup (independent of the rest)
+    const int64_t n4 = (int64_t)nq * lq * dim / 4;
+    const int64_t per = (n4 + gridDim.x - 1) / gridDim.x;
+    const int64_t i0 = per * blockIdx.x;
+    grad_q_sum_ranges(dq_part, dq_R, i0, i0 + per < n4 ? i0 + per : n4, n4, dq);
+  }
   const int E = nq * lq;
-  const GdLds L = gd_lds(E, nq, dim);
+  const GdLds L = gd_lds(E, nq, RPP);  // the same layout the launcher sized for this TPR
   uint16_t* am = reinterpret_cast<uint16_t*>(gd_smem + L.keys);
   uint16_t* sorted = reinterpret_cast<uint16_t*>(gd_smem + L.sorted);
   int* cnt = reinterpret_cast<int*>(gd_smem + L.cnt);
@@ -467,49 +492,54 @@ int grad_q_ranges(int64_t n_docs, int64_t n_tok, int64_t E, int dim) {
 
 hipError_t launch_grad_q(const uint16_t* d_tok, const int64_t* off, int64_t n_docs, int64_t n_tok,
                          int dim, int nq, int lq, const uint16_t* amax, const float* G,
-                         float* part, float* dq, hipStream_t stream) {
+                         float* part, float* dq, bool defer_sum, hipStream_t stream) {
   const int64_t E = (int64_t)nq * lq;
   const int R = grad_q_ranges(n_docs, n_tok, E, dim);
   const int n_groups = (int)((E + kGqEntries - 1) / kGqEntries);
   const unsigned blocks = (unsigned)((int64_t)n_groups * R);
   if (dim <= 128)
     hipLaunchKernelGGL(grad_q_part_kernel<1>, dim3(blocks), dim3(kGqThreads), 0, stream, d_tok,
-                       off, n_docs, n_tok, dim, nq, lq, amax, G, part, n_groups, R);
+                       off, n_docs, n_tok, dim, nq, lq, amax, G, part, dq, n_groups, R);
   else
     hipLaunchKernelGGL(grad_q_part_kernel<2>, dim3(blocks), dim3(kGqThreads), 0, stream, d_tok,
-                       off, n_docs, n_tok, dim, nq, lq, amax, G, part, n_groups, R);
-  const int64_t n4 = E * dim / 4;
-  hipLaunchKernelGGL(grad_q_reduce_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0,
-                     stream, part, R, n4, dq);
+                       off, n_docs, n_tok, dim, nq, lq, amax, G, part, dq, n_groups, R);
+  if (R > 1 && !defer_sum) {
+    const int64_t n4 = E * dim / 4;
+    hipLaunchKernelGGL(grad_q_reduce_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0,
+                       stream, part, R, n4, dq);
+  }
   return hipGetLastError();
 }
 
 template <int TPR>
 hipError_t launch_grad_d_t(const uint16_t* q, const int64_t* off, int64_t n_docs, int64_t n_tok,
                            int dim, int nq, int lq, uint64_t magic, const uint16_t* amax,
-                           const float* G, float* dd, int lds, hipStream_t stream) {
+                           const float* G, float* dd, const float* dq_part, int dq_R, float* dq,
+                           hipStream_t stream) {
+  const int lds = gd_lds(nq * lq, nq, kGdThreads / TPR).total;
   if (lds > 65536) {  // beyond the default dynamic LDS limit (large nq * lq only)
     const hipError_t e = hipFuncSetAttribute((const void*)grad_d_kernel<TPR>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(grad_d_kernel<TPR>, dim3((unsigned)n_docs), dim3(kGdThreads), lds, stream, q,
-                     off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd);
+                     off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq);
   return hipGetLastError();
 }
 
 hipError_t launch_grad_d(const uint16_t* q, const int64_t* off, int64_t n_docs, int64_t n_tok,
                          int dim, int nq, int lq, const uint16_t* amax, const float* G, float* dd,
-                         hipStream_t stream) {
-  const int E = nq * lq;
-  const int lds = gd_lds(E, nq, dim).total;
+                         const float* dq_part, float* dq, hipStream_t stream) {
+  const int dq_R = dq_part ? grad_q_ranges(n_docs, n_tok, (int64_t)nq * lq, dim) : 0;
+  if (dq_R <= 1) dq_part = nullptr;  // one range: grad_q wrote the final sums
   // floor(e / lq) = (e * ceil(2^32 / lq)) >> 32 for e < 2^14 and lq <= 128: the product
   // overshoots e / lq by less than e / 2^32 < 2^-18, below the 1 / lq gap to the next integer.
   const uint64_t magic = (0x100000000ull + (uint64_t)lq - 1) / (uint64_t)lq;
   switch (gd_tpr(dim)) {
-    case 2: return launch_grad_d_t<2>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, lds, stream);
-    case 4: return launch_grad_d_t<4>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, lds, stream);
-    default: return launch_grad_d_t<8>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, lds, stream);
+    case 2: return launch_grad_d_t<2>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, stream);
+    case 4: return launch_grad_d_t<4>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, stream);
+    case 8: return launch_grad_d_t<8>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, stream);
+    default: return hipErrorInvalidValue;
   }
 }
 

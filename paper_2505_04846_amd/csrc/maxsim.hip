@@ -397,9 +397,10 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_occupancy<KS, ARGMAX>())) void ma
 }
 
 __global__ void partition_kernel(const int64_t* off, int64_t n_docs, int64_t n_tok, int R,
-                                 int64_t* part, int32_t* ctrl) {
+                                 int64_t* part, int32_t* ctrl, int n_ctrl) {
   const int r = blockIdx.x * blockDim.x + threadIdx.x;
-  if (r < 2 && ctrl) ctrl[r] = 0;
+  if (ctrl)
+    for (int i = r; i < n_ctrl; i += gridDim.x * blockDim.x) ctrl[i] = 0;
   if (r > R) return;
   if (r == R) {
     part[r] = n_docs;
@@ -495,11 +496,11 @@ bool maxsim_plan(int nq, int lq, int64_t n_docs, int64_t n_tok, int dim, bool ar
 }
 
 hipError_t launch_partition(const int64_t* off, int64_t n_docs, int64_t n_tok, int n_ranges,
-                            int64_t* part, int32_t* ctrl, hipStream_t stream) {
+                            int64_t* part, int32_t* ctrl, int n_ctrl, hipStream_t stream) {
   const int threads = 256;
   const int blocks = (n_ranges + 1 + threads - 1) / threads;
   hipLaunchKernelGGL(partition_kernel, dim3(blocks), dim3(threads), 0, stream, off, n_docs,
-                     n_tok, n_ranges, part, ctrl);
+                     n_tok, n_ranges, part, ctrl, n_ctrl);
   return hipGetLastError();
 }
 

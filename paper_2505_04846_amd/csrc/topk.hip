@@ -31,7 +31,7 @@ constexpr int kWaves = kThreads / kWave;
 constexpr int kMaxK = 1024;
 constexpr int kCap = 8192;      // LDS candidate list (keys and indices: 64 KiB)
 constexpr int kSamples = 4096;  // 64 runs of 64 consecutive entries
-constexpr int kUnroll = 8;      // loads in flight per thread while streaming
+constexpr int kUnroll = 8;      // 16-byte loads in flight per thread while streaming
 
 __device__ __forceinline__ unsigned long long key64(uint32_t key, uint32_t idx) {
   return ((unsigned long long)key << 32) | (unsigned long long)(~idx);
@@ -165,24 +165,40 @@ __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float* __rest
                               need);
     if (tid == 0) n_cand = 0;
     __syncthreads();
-    // 2. stream the row once, appending the entries at or above t
-    for (int64_t base = 0; base < n; base += (int64_t)kThreads * kUnroll) {
-      float v[kUnroll];
+    // 2. stream the row once, appending the entries at or above t: 16-byte loads from the
+    //    first 16-byte boundary of the row (kUnroll of them in flight per thread), the few
+    //    entries before it and after the last whole vector one by one
+    auto offer = [&](float v, int64_t i) {
+      const uint32_t key = score_key(v);
+      if (key >= t) {
+        const uint32_t p = atomicAdd(&n_cand, 1u);
+        if (p < kCap) {
+          ckey[p] = key;
+          cidx[p] = (uint32_t)i;
+        }
+      }
+    };
+    const int64_t head = (int64_t)((16u - (uint32_t)(reinterpret_cast<uintptr_t>(x) & 15u)) & 15u) / 4;
+    const int64_t nv = (n - head) / 4;  // whole 16-byte vectors (n > kCap > head)
+    const f32x4* xv = reinterpret_cast<const f32x4*>(x + head);
+    if (tid < head) offer(x[tid], tid);
+    for (int64_t i = head + 4 * nv + tid; i < n; i += kThreads) offer(x[i], i);
+    for (int64_t base = 0; base < nv; base += (int64_t)kThreads * kUnroll) {
+      f32x4 v[kUnroll];
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
-        const int64_t i = base + (int64_t)u * kThreads + tid;
-        v[u] = i < n ? x[i] : 0.f;
+        const int64_t j = base + (int64_t)u * kThreads + tid;
+        v[u] = j < nv ? xv[j] : f32x4{0.f, 0.f, 0.f, 0.f};
       }
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
-        const int64_t i = base + (int64_t)u * kThreads + tid;
-        const uint32_t key = score_key(v[u]);
-        if (i < n && key >= t) {
-          const uint32_t p = atomicAdd(&n_cand, 1u);
-          if (p < kCap) {
-            ckey[p] = key;
-            cidx[p] = (uint32_t)i;
-          }
+        const int64_t j = base + (int64_t)u * kThreads + tid;
+        if (j < nv) {
+          const int64_t i = head + 4 * j;
+          offer(v[u].x, i);
+          offer(v[u].y, i + 1);
+          offer(v[u].z, i + 2);
+          offer(v[u].w, i + 3);
         }
       }
     }
