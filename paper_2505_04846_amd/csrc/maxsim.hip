@@ -477,13 +477,13 @@ bool maxsim_plan(int nq, int lq, int64_t n_docs, int64_t n_tok, int dim, bool ar
   p->qpw = p->nb * 32 / p->lqp;
   const int64_t q_per_wg = (int64_t)p->qpw * p->wpw;
   p->n_qgroups = (int)((nq + q_per_wg - 1) / q_per_wg);
-  // Workgroups: the plain score takes enough to fill every CU's two resident slots eight times
+  // Workgroups: the plain score takes enough to fill every CU's two resident slots 32 times
   // over (short ranges keep the workgroups sharing a range in step, so the range is served from
   // L2); the argmax variant, whose stores are short, takes one round of resident workgroups
   // (fewer per-workgroup prologues).  No range is shorter than ~1024 tokens (the query operands
   // are re-loaded by every workgroup).
   const int occ = 2;  // resident workgroups per CU
-  const int64_t target_wg = (int64_t)(n_cu > 0 ? n_cu : 256) * occ * (argmax ? 1 : 8);
+  const int64_t target_wg = (int64_t)(n_cu > 0 ? n_cu : 256) * occ * (argmax ? 1 : 32);
   int64_t R = (target_wg + p->n_qgroups - 1) / p->n_qgroups;
   const int64_t max_by_tokens = n_tok / 1024 > 0 ? n_tok / 1024 : 1;
   if (R > max_by_tokens) R = max_by_tokens;

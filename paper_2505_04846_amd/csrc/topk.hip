@@ -4,9 +4,9 @@
 // to break ties by lower index, the 64-bit key (score key << 32) | ~index (unique per row).
 //
 // Fast path (one pass over the row):
-//   1. Sample.  4096 scores from 64 evenly spaced runs of the row; the s-th largest sample key
-//      t (s chosen so that about 1.5 k + 12 n / 4096 row entries are expected at or above it)
-//      is found by a radix select in LDS.
+//   1. Sample.  About one score in 64 (up to 16384), in evenly spaced runs of 64 entries; the
+//      s-th largest sample key t (s chosen so that the expected number of row entries at or
+//      above t lies well inside [k, kCap], see below) is found by a radix select in LDS.
 //   2. Stream.  Every entry with key >= t is appended to an LDS candidate list (kCap entries).
 //      If t is too high (fewer than k candidates) or the list overflows, the row takes the slow
 //      path.  Otherwise the candidates contain the top-k: any other entry is below t and at
@@ -30,7 +30,7 @@ constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kMaxK = 1024;
 constexpr int kCap = 8192;      // LDS candidate list (keys and indices: 64 KiB)
-constexpr int kSamples = 4096;  // 64 runs of 64 consecutive entries
+constexpr int kMaxRuns = 2 * kCap / 64;  // sample: up to 256 runs of 64 entries (16384 keys)
 constexpr int kUnroll = 8;      // 16-byte loads in flight per thread while streaming
 
 __device__ __forceinline__ unsigned long long key64(uint32_t key, uint32_t idx) {
@@ -130,8 +130,11 @@ __device__ void sort_and_write(unsigned long long* sk, uint32_t k, int64_t row, 
 __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float* __restrict__ S,
                                                              int64_t n, int64_t ld, int k,
                                                              float* out_s, int64_t* out_i) {
-  __shared__ uint32_t ckey[kCap];  // candidate keys (the sample first)
-  __shared__ uint32_t cidx[kCap];  // candidate indices
+  // candidate keys (ckey) and indices (cidx); before the stream, the whole buffer holds the
+  // sample's keys
+  __shared__ uint32_t cbuf[2 * kCap];
+  uint32_t* ckey = cbuf;
+  uint32_t* cidx = cbuf + kCap;
   __shared__ unsigned long long sk[kMaxK];
   __shared__ uint32_t hist[256];
   __shared__ uint32_t sh[4];
@@ -153,16 +156,32 @@ __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float* __rest
     if (tid == 0) n_cand = (uint32_t)n;
     __syncthreads();
   } else {
-    // 1. sample: run r covers entries [r * n / 64, + 64) -- n > kCap, so runs do not overlap
-    for (int s = tid; s < kSamples; s += kThreads) {
-      const int64_t i = (int64_t)(s >> 6) * n / 64 + (s & 63);
-      ckey[s] = score_key(x[i]);
+    // 1. sample: nr runs of 16 aligned 16-byte vectors (64 entries), run r starting at vector
+    //    r * nv / nr of the row's aligned part (nv >= 16 nr, so runs do not overlap); about one
+    //    entry in 64 is sampled, at most kMaxRuns runs.
+    const int64_t head = (int64_t)((16u - (uint32_t)(reinterpret_cast<uintptr_t>(x) & 15u)) & 15u) / 4;
+    const int64_t nv = (n - head) / 4;  // whole 16-byte vectors (n > kCap > head)
+    const f32x4* xv = reinterpret_cast<const f32x4*>(x + head);
+    const int nr = (n + 4095) / 4096 < kMaxRuns ? (int)((n + 4095) / 4096) : kMaxRuns;
+    const int ns = 64 * nr;
+    for (int u = tid; u < 16 * nr; u += kThreads) {
+      const f32x4 v = xv[(int64_t)(u >> 4) * nv / nr + (u & 15)];
+      cbuf[4 * u] = score_key(v.x);
+      cbuf[4 * u + 1] = score_key(v.y);
+      cbuf[4 * u + 2] = score_key(v.z);
+      cbuf[4 * u + 3] = score_key(v.w);
     }
-    const uint32_t want = (uint32_t)((3ll * k * kSamples + 2 * n - 1) / (2 * n)) + 12u;
+    // The threshold is the want-th largest sample key: about want * n / ns row entries reach it,
+    // with a relative spread of about 1 / sqrt(want).  want = 64 gives 4096 +- 512 expected
+    // candidates when ns = n / 64 -- six standard deviations inside [1024, kCap], hence
+    // [k, kCap] for every k -- and fewer sample keys keep the expected count at 4096 on rows
+    // longer than kMaxRuns * 4096 (at a wider spread).
+    int64_t want = (int64_t)ceil(4096.0 * ns / (double)n);
+    want = want > 64 ? 64 : (want < 16 ? 16 : want);
     uint32_t t;
     uint32_t need;
-    radix_select<4, uint32_t>([&](int64_t i) { return ckey[i]; }, kSamples, want, hist, sh, t,
-                              need);
+    radix_select<4, uint32_t>([&](int64_t i) { return cbuf[i]; }, ns, (uint32_t)want, hist, sh,
+                              t, need);
     if (tid == 0) n_cand = 0;
     __syncthreads();
     // 2. stream the row once, appending the entries at or above t: 16-byte loads from the
@@ -178,9 +197,6 @@ __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float* __rest
         }
       }
     };
-    const int64_t head = (int64_t)((16u - (uint32_t)(reinterpret_cast<uintptr_t>(x) & 15u)) & 15u) / 4;
-    const int64_t nv = (n - head) / 4;  // whole 16-byte vectors (n > kCap > head)
-    const f32x4* xv = reinterpret_cast<const f32x4*>(x + head);
     if (tid < head) offer(x[tid], tid);
     for (int64_t i = head + 4 * nv + tid; i < n; i += kThreads) offer(x[i], i);
     for (int64_t base = 0; base < nv; base += (int64_t)kThreads * kUnroll) {

@@ -210,29 +210,27 @@ def test_topk_long_row_of_equal_scores_takes_exact_path():
 
 
 def test_topk_unrepresentative_sample_takes_exact_path():
-    # the documents the sampler reads (64 runs of 64 at r * n / 64) score highest and are the
-    # only high ones: the threshold then admits fewer than k candidates and the exact path runs
-    n, k = 10000, 200
-    sampled = set()
-    for sidx in range(4096):
-        sampled.add((sidx >> 6) * n // 64 + (sidx & 63))
+    # the documents the sampler reads (nr = ceil(n / 4096) runs of 64 starting at 16-byte
+    # vector r * (n / 4) / nr of the row, which is 16-byte aligned here) score highest and are
+    # the only high ones: the threshold then admits fewer than k candidates and the exact path
+    # runs
+    n, k, lq, dim = 300_000, 1000, 4, 32
+    nv, nr = n // 4, min(256, (n + 4095) // 4096)
+    sampled = np.array(sorted({4 * ((u >> 4) * nv // nr + (u & 15)) + c
+                               for u in range(16 * nr) for c in range(4)}))
     g = torch.Generator().manual_seed(5)
-    Q = synth.unit_rows(4, 32, g, "cpu", torch.bfloat16).reshape(1, 4, 32)
-    low = synth.unit_rows(n, 32, g, "cpu", torch.bfloat16)
-    noise = synth.unit_rows(n * 4, 32, g, "cpu", torch.float32).reshape(n, 4, 32)
-    docs = []
-    for d in range(n):
-        if d in sampled:  # the query's tokens, perturbed per document: distinct high scores
-            docs.append(synth._normalise(Q[0].float() + 0.3 * noise[d]).to(torch.bfloat16))
-        else:
-            docs.append(low[d:d + 1])
-    lens = torch.tensor([t.shape[0] for t in docs])
-    D = torch.cat(docs)
-    off = synth.csr_offsets(lens)
+    Q = synth.unit_rows(lq, dim, g, "cpu", torch.bfloat16).reshape(1, lq, dim)
+    D = synth.unit_rows(n, dim, g, "cpu", torch.float32)
+    noise = synth.unit_rows(sampled.size, dim, g, "cpu", torch.float32)
+    qsum = Q[0].float().sum(0)
+    D[torch.as_tensor(sampled)] = synth._normalise(qsum[None] / qsum.norm() + 0.3 * noise)
+    D = D.to(torch.bfloat16)
+    off = synth.csr_offsets(torch.ones(n, dtype=torch.int64))
     s, i = hpr.maxsim_topk(*_to_dev(Q, D, off), k)
-    O = oracle.maxsim_scores(_bf(Q), _bf(D), off.numpy())
-    r = check_topk(s.cpu().numpy()[0], i.cpu().numpy()[0], O[0], k)
-    assert set(i.cpu().numpy()[0].tolist()) <= sampled
+    # one token per document: the MaxSim score is <sum_i q_i, d> (the pinned Ld = 1 closed form)
+    O = oracle.dense_scores(_bf(Q)[0].sum(0)[None], _bf(D))
+    check_topk(s.cpu().numpy()[0], i.cpu().numpy()[0], O[0], k)
+    assert set(i.cpu().numpy()[0].tolist()) <= set(sampled.tolist())
 
 # ------------------------------------------------------------------------------ InfoNCE loss
 
