@@ -16,7 +16,7 @@
 //      rows [S, n) are rescanned for those queries only, until no list overflows.
 //
 // GEMM tile: 256 queries x 256 rows per 8-wave workgroup (each wave 64 x 128 = 2 x 4 blocks of
-// v_mfma_f32_32x32x16_f16); K advances 32 halves per stage through a 4-deep LDS ring filled by
+// v_mfma_f32_32x32x16_f16; 128 x 128 per wave at one wave per SIMD measured 20 % slower); K advances 32 halves per stage through a 4-deep LDS ring filled by
 // direct-to-LDS loads (global_load_lds_dwordx4, a wave-uniform base plus 32-bit lane offsets),
 // so two to three stages of loads are in flight while one is multiplied.  The loop is software
 // pipelined with one barrier per stage, placed between the stage's two k-steps: the next
@@ -39,7 +39,11 @@ constexpr int kTQ = 256;       // queries per workgroup tile
 constexpr int kTR = 256;       // rows per workgroup tile
 constexpr int kKC = 32;        // halves of K per stage
 constexpr int kStages = 4;     // LDS ring depth
-constexpr int kGemmWaves = 8;  // 4 along queries x 2 along rows
+constexpr int kWQ = 4;         // waves along queries
+constexpr int kWR = 2;         // waves along rows
+constexpr int kBQ = kTQ / (32 * kWQ);  // 32-query blocks per wave
+constexpr int kBR = kTR / (32 * kWR);  // 32-row blocks per wave
+constexpr int kGemmWaves = kWQ * kWR;
 constexpr int kGemmThreads = 64 * kGemmWaves;
 constexpr int kRowBytes = kKC * 2;                      // 64
 constexpr int kTileBytes = kTQ * kRowBytes;             // 16 KiB per operand per stage
@@ -48,6 +52,10 @@ constexpr int kLoadsPerWave = kStageBytes / 1024 / kGemmWaves;  // 16-byte loads
 
 // 16 zero bytes in global memory: the source of the K-tail chunks past `dim`.
 __device__ __attribute__((aligned(16))) const uint32_t kZero16[4] = {0u, 0u, 0u, 0u};
+
+// s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+constexpr int kWaitLgkm0 = 15 | (3 << 14) | (7 << 4);
 
 struct GemmArgs {
   const uint16_t* q;      // fp16 [nqa, dim]
@@ -75,8 +83,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void dense_gemm_kernel(GemmArgs a)
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wq = wave & 3;   // 64-query slice of the tile
-  const int wr = wave >> 2;  // 128-row slice of the tile
+  const int wq = wave % kWQ;  // (32 kBQ)-query slice of the tile
+  const int wr = wave / kWQ;  // (32 kBR)-row slice of the tile
 
   const int64_t total = (int64_t)a.n_qt * a.n_rt;
   const int64_t lin = xcd_linear(blockIdx.x, total);
@@ -135,27 +143,27 @@ __global__ __launch_bounds__(kGemmThreads, 1) void dense_gemm_kernel(GemmArgs a)
 
   // ---- per-lane LDS offsets of the MFMA operands: row `col` of block b, chunk 2 s + half
   const int col = lane & 31, half = lane >> 5;
-  uint32_t offq[2][2], offx[4][2];
+  uint32_t offq[kBQ][2], offx[kBR][2];
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
     const int c = 2 * s + half;
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int r = wq * 64 + 32 * b + col;
+    for (int b = 0; b < kBQ; ++b) {
+      const int r = wq * 32 * kBQ + 32 * b + col;
       offq[b][s] = r * kRowBytes + 16 * (c ^ ((r >> 2) & 3));
     }
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int r = wr * 128 + 32 * b + col;
+    for (int b = 0; b < kBR; ++b) {
+      const int r = wr * 32 * kBR + 32 * b + col;
       offx[b][s] = kTileBytes + r * kRowBytes + 16 * (c ^ ((r >> 2) & 3));
     }
   }
 
-  f32x16 acc[2][4];
+  f32x16 acc[kBQ][kBR];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < kBQ; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < kBR; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
@@ -167,20 +175,20 @@ __global__ __launch_bounds__(kGemmThreads, 1) void dense_gemm_kernel(GemmArgs a)
   for (int s = 0; s < kStages - 1; ++s) issue_stage(s, s < nk ? s : nk - 1);
 
   struct Frags {
-    f16x8 a[2], b[4];
+    f16x8 a[kBQ], b[kBR];
   };
   auto read_frags = [&](int kk, int s, Frags& f) {
     const unsigned char* st = smem + (kk % kStages) * kStageBytes;
 #pragma unroll
-    for (int b = 0; b < 2; ++b) f.a[b] = as_f16x8(*reinterpret_cast<const u32x4*>(st + offq[b][s]));
+    for (int b = 0; b < kBQ; ++b) f.a[b] = as_f16x8(*reinterpret_cast<const u32x4*>(st + offq[b][s]));
 #pragma unroll
-    for (int b = 0; b < 4; ++b) f.b[b] = as_f16x8(*reinterpret_cast<const u32x4*>(st + offx[b][s]));
+    for (int b = 0; b < kBR; ++b) f.b[b] = as_f16x8(*reinterpret_cast<const u32x4*>(st + offx[b][s]));
   };
   auto mfma = [&](const Frags& f) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < kBQ; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < kBR; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
   };
   auto barrier = [&]() {
@@ -190,7 +198,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void dense_gemm_kernel(GemmArgs a)
   };
 
   Frags f0, f1;
-  __builtin_amdgcn_s_waitcnt(0x0f70 | (2 * kLoadsPerWave));  // stage 0 landed (this wave)
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * kLoadsPerWave));  // stage 0 landed (this wave)
   barrier();                                                // ... and for every wave
   read_frags(0, 0, f0);
 #pragma unroll 1
@@ -200,8 +208,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void dense_gemm_kernel(GemmArgs a)
     // Stage kk+1 lands everywhere, and every wave's reads of stage kk-1 are complete (this
     // wave's LDS reads drain before the barrier), so that stage's buffer ((kk + 3) % 4) can
     // take stage kk+3.
-    __builtin_amdgcn_s_waitcnt(0x0f70 | kLoadsPerWave);
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(kLoadsPerWave));
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     barrier();
     const int nxt = kk + kStages - 1;
     issue_stage(nxt, nxt < nk ? nxt : nk - 1);
@@ -209,21 +217,21 @@ __global__ __launch_bounds__(kGemmThreads, 1) void dense_gemm_kernel(GemmArgs a)
     __builtin_amdgcn_sched_barrier(0);  // the next stage's reads go out before these MFMAs
     mfma(f1);
   }
-  __builtin_amdgcn_s_waitcnt(0x0f70);  // no load may still target LDS when the kernel ends
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no load may still target LDS when the kernel ends
 
-  // ---- epilogue.  acc[i][j] register r: query q_base + 64 wq + 32 i + 8 (r / 4) + 4 half
-  // + r % 4, row row_base + 128 wr + 32 j + col.
+  // ---- epilogue.  acc[i][j] register r: query q_base + 32 kBQ wq + 32 i + 8 (r / 4) +
+  // 4 half + r % 4, row row_base + 32 kBR wr + 32 j + col.
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < kBQ; ++i) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int ql = q_base + 64 * wq + 32 * i + 8 * (r >> 2) + 4 * half + (r & 3);
+      const int ql = q_base + 32 * kBQ * wq + 32 * i + 8 * (r >> 2) + 4 * half + (r & 3);
       if (ql >= a.nqa) continue;
       if (!FILTER) {
-        float* dst = a.scores + (int64_t)ql * a.ld + (row_base - a.r0) + 128 * wr + col;
+        float* dst = a.scores + (int64_t)ql * a.ld + (row_base - a.r0) + 32 * kBR * wr + col;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int64_t row = row_base + 128 * wr + 32 * j + col;
+        for (int j = 0; j < kBR; ++j) {
+          const int64_t row = row_base + 32 * kBR * wr + 32 * j + col;
           if (row < a.r1) dst[32 * j] = acc[i][j][r];
         }
       } else {
@@ -231,8 +239,8 @@ __global__ __launch_bounds__(kGemmThreads, 1) void dense_gemm_kernel(GemmArgs a)
         const float th = a.theta[gq];
         const int64_t tie = a.tie[gq];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int64_t row = row_base + 128 * wr + 32 * j + col;
+        for (int j = 0; j < kBR; ++j) {
+          const int64_t row = row_base + 32 * kBR * wr + 32 * j + col;
           const float v = acc[i][j][r];
           if (row < a.r1 && (v > th || (v == th && row <= tie))) {
             const int p = atomicAdd(&a.count[gq], 1);

@@ -38,9 +38,12 @@ __device__ __forceinline__ unsigned long long key64(uint32_t key, uint32_t idx) 
 }
 
 // Finds, among the `m` values produced by get(i), the `want`-th largest under the digits of
-// `bits`-bit keys (most significant digit first, 8 bits per pass).  Returns (prefix, needed):
-// the key itself and how many entries equal to it complete the count.
-template <int PASSES, class K, class Get>
+// `bits`-bit keys (most significant digit first, 8 bits per pass).  Returns (key, needed): the
+// want-th largest key K itself and how many entries equal to K complete the count.  With
+// EARLY, a pass that finds the digit bin holding the want-th entry to hold exactly the entries
+// still needed stops there and returns the bin's lowest possible key instead: then exactly
+// `want` entries have key >= K (for callers that select by key >= K only).
+template <int PASSES, bool EARLY, class K, class Get>
 __device__ void radix_select(Get get, int64_t m, uint32_t want, uint32_t* hist, uint32_t* sh,
                              K& out_key, uint32_t& out_need) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -90,7 +93,9 @@ __device__ void radix_select(Get get, int64_t m, uint32_t want, uint32_t* hist, 
     prefix |= (K)sh[0] << shift;
     pmask |= (K)255u << shift;
     remaining -= sh[1];
+    const bool whole_bin = EARLY && hist[sh[0]] == remaining;  // uniform
     __syncthreads();
+    if (whole_bin) break;  // every entry of the bin is needed: its lowest key is the bound
   }
   out_key = prefix;
   out_need = remaining;
@@ -180,7 +185,7 @@ __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float* __rest
     want = want > 64 ? 64 : (want < 16 ? 16 : want);
     uint32_t t;
     uint32_t need;
-    radix_select<4, uint32_t>([&](int64_t i) { return cbuf[i]; }, ns, (uint32_t)want, hist, sh,
+    radix_select<4, true, uint32_t>([&](int64_t i) { return cbuf[i]; }, ns, (uint32_t)want, hist, sh,
                               t, need);
     if (tid == 0) n_cand = 0;
     __syncthreads();
@@ -227,7 +232,7 @@ __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float* __rest
     const uint32_t m = n_cand;
     unsigned long long K;
     uint32_t need;
-    radix_select<8, unsigned long long>([&](int64_t i) { return key64(ckey[i], cidx[i]); }, m,
+    radix_select<8, true, unsigned long long>([&](int64_t i) { return key64(ckey[i], cidx[i]); }, m,
                                         (uint32_t)k, hist, sh, K, need);
     if (tid == 0) n_cand = 0;  // reused as the gather counter
     __syncthreads();
@@ -245,7 +250,7 @@ __global__ __launch_bounds__(kThreads) void topk_rows_kernel(const float* __rest
   // ---- slow path: exact select over the row in global memory
   uint32_t K;
   uint32_t need_eq;
-  radix_select<4, uint32_t>([&](int64_t i) { return score_key(x[i]); }, n, (uint32_t)k, hist,
+  radix_select<4, false, uint32_t>([&](int64_t i) { return score_key(x[i]); }, n, (uint32_t)k, hist,
                             sh, K, need_eq);
   const uint32_t n_gt = (uint32_t)k - need_eq;  // entries strictly above K
   if (tid == 0) n_cand = 0;
