@@ -14,6 +14,8 @@ Contents
   maxsim_scores, maxsim_argmax late-interaction similarity (Sec. 2.2, Sec. 3.2.1, Fig. 3B)
   rank_topk                    exact top-k by (score desc, index asc) (Sec. 2.3 nearest neighbours)
   coltrast_li_loss             InfoNCE over MaxSim scores and its gradients (Sec. 3.2.1, L_LI)
+  contrastive_loss             InfoNCE over cosines of mean-pooled embeddings (Sec. 3.2.1, L_C)
+  coltrast_total_loss          L = (L_LI + L_C) / 2 and its gradients (Sec. 3.2.1)
   dense_scores, dense_topk     inner-product / cosine retrieval on pooled embeddings (Sec. 3.2.1,
                                Sec. 4.2)
 
@@ -24,6 +26,7 @@ fixtures, closed forms, invariants, brute force on tiny inputs and finite differ
 from .bits import decode_bf16, decode_fp16
 from .maxsim import maxsim_scores, maxsim_argmax, rank_topk
 from .loss import coltrast_li_loss
+from .contrastive import contrastive_loss, coltrast_total_loss, pooled_means
 from .dense import dense_scores, dense_topk
 
 __all__ = [
@@ -33,6 +36,9 @@ __all__ = [
     "maxsim_argmax",
     "rank_topk",
     "coltrast_li_loss",
+    "contrastive_loss",
+    "coltrast_total_loss",
+    "pooled_means",
     "dense_scores",
     "dense_topk",
 ]
