@@ -9,6 +9,9 @@
  *   maxsim_topk            exact top-k documents per query under MaxSim.
  *   coltrast_loss_fwd_bwd  in-batch InfoNCE loss over MaxSim scores (the L_LI half of the
  *                          ColTrast loss) with its gradients.
+ *   coltrast_total_loss_fwd_bwd
+ *                          the whole ColTrast loss (L_LI + L_C) / 2, L_C being a contrastive
+ *                          loss on the cosines of mean-pooled embeddings, with its gradients.
  *   dense_ip_topk          exact top-k rows of a pooled-embedding store by inner product
  *                          (= cosine for L2-normalised rows).
  *
@@ -66,8 +69,9 @@ typedef int32_t hpr_status;
  *     dim <= 256; coltrast_loss_fwd_bwd: lq <= 64 when dim <= 128, lq <= 32 when dim <= 256;
  *     n_tok < 2^31 (a store of 2^31 bf16 tokens of dim 128 would not fit one GPU's HBM).
  *   Top-k: 1 <= k <= min(n, 1024) (k outside that range is HPR_ERR_INVALID_ARG).
- *   coltrast_loss_fwd_bwd: nq * lq <= 16384 and every document has at most 65536 tokens (the
- *     latter is checked on the device: a longer document makes *loss NaN).
+ *   coltrast_loss_fwd_bwd and coltrast_total_loss_fwd_bwd: the same lq limits, nq * lq <= 16384
+ *     and every document has at most 65536 tokens (the latter is checked on the device: a
+ *     longer document makes the loss NaN).
  *   dense_ip_topk: dim % 8 == 0, 8 <= dim <= 8192; n < 2^31.
  */
 
@@ -143,6 +147,40 @@ hpr_status coltrast_loss_fwd_bwd(const uint16_t* q, int32_t nq, int32_t lq,
                                  void* ws, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------------------------
+ * coltrast_total_loss_fwd_bwd -- the whole ColTrast loss L = (L_LI + L_C) / 2, forward and
+ * backward.
+ *
+ * The paper trains its encoder on the mean of two losses (Sec. 3.2.1, "Embedding performance:
+ * loss function"): L_LI, the MaxSim loss of coltrast_loss_fwd_bwd, and L_C, SimCSE's
+ * contrastive loss applied to pooled embeddings and compared by cosine (same section,
+ * "Similarity metric").  Pooling is the mean over a sequence's tokens, and L_C compares each
+ * query with every in-batch document, with the positives of L_LI:
+ *     P_q = (1/lq) sum_i Q[q,i,:];   P_d = (1/L_d) sum_{j in d} D[j,:]   (L_d: d's token count)
+ *     c[q,d] = <P_q, P_d> / (|P_q| |P_d| temperature)
+ *     L_C = (1/nq) sum_q ( log sum_d exp(c[q,d]) - c[q, pos_idx[q]] )
+ * The gradients are those of L with respect to the bf16 inputs taken as real numbers: half the
+ * gradients of coltrast_loss_fwd_bwd plus half those of L_C, the latter the same for every token
+ * of a query (or of a document).  Arithmetic: pooled sums and cosines in fp32, in a fixed order;
+ * repeated calls give identical bits.
+ *
+ *   pos_idx      int32 [nq] positives; an out-of-range entry makes all three losses NaN.
+ *   logit_scale  the inverse temperature of L_LI (finite).
+ *   temperature  the temperature of L_C (> 0, finite, with a finite fp32 inverse; 0.05 in
+ *                SimCSE).
+ *   loss         fp32 [3] output: (L, L_LI, L_C) (stays on the device).
+ *   dq           fp32 [nq, lq, dim] output, or NULL to skip it.
+ *   dd           fp32 [n_tok, dim] output (every row written), or NULL to skip it.
+ *   ws           workspace of coltrast_total_loss_workspace_size(...) bytes.
+ * A pooled embedding of zero norm (an all-zero query or document) gives NaN.
+ * ------------------------------------------------------------------------------------------- */
+hpr_status coltrast_total_loss_fwd_bwd(const uint16_t* q, int32_t nq, int32_t lq,
+                                       const uint16_t* d_tok, const int64_t* d_off,
+                                       int64_t n_docs, int64_t n_tok, int32_t dim,
+                                       const int32_t* pos_idx, float logit_scale,
+                                       float temperature, float* loss, float* dq, float* dd,
+                                       void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------------------------
  * dense_ip_topk -- exact top-k rows of a pooled-embedding store by inner product.
  *
  * At query time the paper ranks chunks by the cosine between the pooled question embedding and
@@ -164,6 +202,8 @@ size_t maxsim_topk_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int64_
                                   int32_t dim, int32_t k);
 size_t coltrast_loss_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int64_t n_tok,
                                     int32_t dim);
+size_t coltrast_total_loss_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int64_t n_tok,
+                                          int32_t dim);
 size_t dense_ip_topk_workspace_size(int32_t nq, int64_t n, int32_t dim, int32_t k);
 
 /* ---------------------------------------------------------------------------------------------
@@ -176,13 +216,14 @@ hpr_status hpr_csr_validate(const int64_t* d_off, int64_t n_docs, int64_t n_tok,
                             void* stream, int64_t* h_first_bad_doc);
 
 /* hpr_scale_f32 -- x[i] *= *scale for i < n (scale is a device scalar); used to apply an
- * upstream gradient to the gradients of coltrast_loss_fwd_bwd without a host round trip. */
+ * upstream gradient to the gradients of the loss calls without a host round trip. */
 hpr_status hpr_scale_f32(float* x, int64_t n, const float* scale, void* stream);
 
 /* Per-kernel timing for benchmarks.  While enabled, every kernel the library launches is
  * bracketed by two HIP events recorded on its launch stream.  hpr_kernel_timing_read
  * synchronises on the events recorded for kernel `name` ("partition", "maxsim",
- * "maxsim_argmax", "topk", "infonce", "grad_q", "grad_d", "dense_scan", "dense_merge"), returns
+ * "maxsim_argmax", "topk", "infonce", "pool", "contrastive", "grad_q", "grad_d",
+ * "dense_sample", "dense_scan", "dense_merge"), returns
  * the sum of their durations in milliseconds and the launch count, and forgets them. */
 hpr_status hpr_kernel_timing(int32_t enable);
 hpr_status hpr_kernel_timing_read(const char* name, double* total_ms, int64_t* launches);

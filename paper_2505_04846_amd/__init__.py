@@ -8,6 +8,9 @@ fallback: if the library is not built, or a call fails, an exception is raised.
     maxsim_topk(Q, D, off, k)                     -> (scores fp32 [nq, k], idx int64 [nq, k])
     coltrast_loss_fwd_bwd(Q, D, off, pos, scale)  -> dict(loss, dq, dd, scores)
     coltrast_loss(Q, D, off, pos, scale)          -> loss with autograd to Q and D
+    coltrast_total_loss_fwd_bwd(Q, D, off, pos, scale, tau)
+                                                  -> dict(loss [3]: L, L_LI, L_C; dq, dd)
+    coltrast_total_loss(Q, D, off, pos, scale, tau) -> L with autograd to Q and D
     dense_ip_topk(Q, X, k)                        -> (scores fp32 [nq, k], idx int64 [nq, k])
     csr_validate(off, n_tok)                      -> (status name, first bad document or -1)
 
@@ -55,10 +58,13 @@ _SIGNATURES = {
     "maxsim_topk": (_I32, [_P, _I32, _I32, _P, _P, _I64, _I64, _I32, _I32, _P, _P, _P, _SZ, _P]),
     "coltrast_loss_fwd_bwd": (_I32, [_P, _I32, _I32, _P, _P, _I64, _I64, _I32, _P, _F32,
                                      _P, _P, _P, _P, _P, _SZ, _P]),
+    "coltrast_total_loss_fwd_bwd": (_I32, [_P, _I32, _I32, _P, _P, _I64, _I64, _I32, _P, _F32,
+                                           _F32, _P, _P, _P, _P, _SZ, _P]),
     "dense_ip_topk": (_I32, [_P, _I32, _P, _I64, _I32, _I32, _P, _P, _P, _SZ, _P]),
     "maxsim_score_workspace_size": (_SZ, [_I32, _I32, _I64, _I64, _I32]),
     "maxsim_topk_workspace_size": (_SZ, [_I32, _I32, _I64, _I64, _I32, _I32]),
     "coltrast_loss_workspace_size": (_SZ, [_I32, _I32, _I64, _I64, _I32]),
+    "coltrast_total_loss_workspace_size": (_SZ, [_I32, _I32, _I64, _I64, _I32]),
     "dense_ip_topk_workspace_size": (_SZ, [_I32, _I64, _I32, _I32]),
     "hpr_csr_validate": (_I32, [_P, _I64, _I64, _P, _P, _P]),
     "hpr_scale_f32": (_I32, [_P, _I64, _P, _P]),
@@ -195,6 +201,42 @@ def coltrast_loss_fwd_bwd(Q, D, off, pos, logit_scale, need_dq=True, need_dd=Tru
     return {"loss": loss, "dq": dq, "dd": dd, "scores": scores}
 
 
+def coltrast_total_workspace(Q, D, off):
+    dev, nq, lq, dim, n_docs, n_tok = _maxsim_inputs(Q, D, off)
+    return _workspace(lib().coltrast_total_loss_workspace_size(nq, lq, n_docs, n_tok, dim), dev)
+
+
+def coltrast_total_loss_fwd_bwd(Q, D, off, pos, logit_scale, temperature, need_dq=True,
+                                need_dd=True, ws=None, out=None):
+    """Loss (fp32 [3]: L, L_LI, L_C), dQ (fp32 like Q or None), dD (fp32 like D or None).
+
+    `out` may hold preallocated outputs {"loss", "dq", "dd"} (reused as given).
+    """
+    dev, nq, lq, dim, n_docs, n_tok = _maxsim_inputs(Q, D, off)
+    _need(pos, "pos", torch.int32, 1, dev)
+    if pos.numel() != nq:
+        raise ValueError("pos must hold one positive per query")
+    L = lib()
+    need = L.coltrast_total_loss_workspace_size(nq, lq, n_docs, n_tok, dim)
+    ws = ws if ws is not None and ws.numel() >= need else _workspace(need, dev)
+    out = {} if out is None else out
+    loss = out.get("loss")
+    if loss is None:
+        loss = torch.empty(3, dtype=torch.float32, device=dev)
+    dq = out.get("dq") if need_dq else None
+    if need_dq and dq is None:
+        dq = torch.empty(Q.shape, dtype=torch.float32, device=dev)
+    dd = out.get("dd") if need_dd else None
+    if need_dd and dd is None:
+        dd = torch.empty(D.shape, dtype=torch.float32, device=dev)
+    with torch.cuda.device(dev):
+        _check(L.coltrast_total_loss_fwd_bwd(_ptr(Q), nq, lq, _ptr(D), _ptr(off), n_docs, n_tok,
+                                             dim, _ptr(pos), float(logit_scale),
+                                             float(temperature), _ptr(loss), _ptr(dq), _ptr(dd),
+                                             _ptr(ws), ws.numel(), _stream(dev)))
+    return {"loss": loss, "dq": dq, "dd": dd}
+
+
 def scale_(x, scale):
     """x *= scale in place (x fp32 contiguous CUDA tensor, scale a 1-element fp32 CUDA tensor)."""
     with torch.cuda.device(x.device):
@@ -227,6 +269,27 @@ class _ColTrastLI(torch.autograd.Function):
 def coltrast_loss(Q, D, off, pos, logit_scale):
     """L_LI as a differentiable scalar (gradients reach Q and D)."""
     return _ColTrastLI.apply(Q, D, off, pos, float(logit_scale))
+
+
+class _ColTrastTotal(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, Q, D, off, pos, logit_scale, temperature):
+        r = coltrast_total_loss_fwd_bwd(Q.detach(), D.detach(), off, pos, logit_scale,
+                                        temperature, need_dq=ctx.needs_input_grad[0],
+                                        need_dd=ctx.needs_input_grad[1])
+        ctx.save_for_backward(*(t for t in (r["dq"], r["dd"]) if t is not None))
+        ctx.has = (r["dq"] is not None, r["dd"] is not None)
+        return r["loss"][0]
+
+    @staticmethod
+    def backward(ctx, grad_out):
+        dq, dd = _ColTrastLI.backward(ctx, grad_out)[:2]
+        return dq, dd, None, None, None, None
+
+
+def coltrast_total_loss(Q, D, off, pos, logit_scale, temperature):
+    """The ColTrast loss (L_LI + L_C) / 2 as a differentiable scalar."""
+    return _ColTrastTotal.apply(Q, D, off, pos, float(logit_scale), float(temperature))
 
 
 def dense_ip_topk(Q, X, k, ws=None):

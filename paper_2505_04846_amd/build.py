@@ -20,7 +20,7 @@ BUILD_DIR = os.path.join(PKG_DIR, "_build")
 LIB_NAME = "libhiperrag.so"
 ARCH = "gfx950"
 
-SOURCES = ["abi.hip", "maxsim.hip", "topk.hip", "loss.hip", "dense.hip"]
+SOURCES = ["abi.hip", "maxsim.hip", "topk.hip", "loss.hip", "contrastive.hip", "dense.hip"]
 
 
 def _hipcc():

@@ -154,6 +154,108 @@ hpr_status run_maxsim(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t*
   return HPR_OK;
 }
 
+// Workspace of the loss calls: S, G, the argmax table, the partition, control words, loss
+// terms and dQ partial sums; with the contrastive half also the pooled rows and their norms,
+// dL_C/dc, its terms and the per-query / per-document gradient parts.
+size_t loss_ws_bytes(int32_t nq, int32_t lq, int64_t n_docs, int64_t n_tok, int32_t dim,
+                     bool contrastive) {
+  if (nq < 1 || lq < 1 || n_docs < 1 || dim < 1) return 0;
+  const size_t sd = align_up((size_t)nq * (size_t)n_docs * sizeof(float));
+  const size_t am = align_up((size_t)n_docs * (size_t)nq * (size_t)lq * sizeof(uint16_t));
+  const int64_t E = (int64_t)nq * lq;
+  const size_t gq = align_up((size_t)grad_q_ranges(n_docs, n_tok, E, dim) * (size_t)E *
+                             (size_t)dim * sizeof(float));
+  size_t b = 2 * sd + am + part_bytes(n_docs) + align_up((size_t)kLossCtrlWords * sizeof(int32_t)) +
+             align_up((size_t)nq * sizeof(float)) + gq;
+  if (contrastive) {
+    const size_t qd = align_up((size_t)nq * (size_t)dim * sizeof(float));
+    const size_t dd = align_up((size_t)n_docs * (size_t)dim * sizeof(float));
+    b += 2 * qd + 2 * dd + 2 * align_up((size_t)nq * sizeof(float)) +
+         align_up((size_t)n_docs * sizeof(float)) + sd;
+  }
+  return b;
+}
+
+// Both loss calls.  tau > 0 adds the contrastive half: L = w L_LI + w L_C with w = 1/2, loss[0..2]
+// = (L, L_LI, L_C); otherwise loss[0] = L_LI.
+hpr_status run_loss(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d_tok,
+                    const int64_t* d_off, int64_t n_docs, int64_t n_tok, int32_t dim,
+                    const int32_t* pos_idx, float logit_scale, float tau, float* loss, float* dq,
+                    float* dd, float* scores, void* ws, size_t ws_bytes, void* stream) {
+  const bool total = tau > 0.f;
+  hpr_status st = check_maxsim_args(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim);
+  if (st == HPR_OK) st = check_lq(lq, dim, true);
+  if (st != HPR_OK) return st;
+  if (!pos_idx || !loss || !ws) return fail(HPR_ERR_INVALID_ARG, "pos_idx, loss and ws must be non-NULL");
+  if (!(logit_scale == logit_scale) || logit_scale > 3.0e38f || logit_scale < -3.0e38f)
+    return fail(HPR_ERR_INVALID_ARG, "logit_scale must be finite");
+  if ((int64_t)nq * lq > 16384)
+    return fail(HPR_ERR_UNSUPPORTED_SHAPE, "nq * lq = %lld exceeds 16384", (long long)nq * lq);
+  if ((dq && !aligned16(dq)) || (dd && !aligned16(dd)))
+    return fail(HPR_ERR_INVALID_ARG, "gradient outputs must be 16-byte aligned");
+  const size_t need = loss_ws_bytes(nq, lq, n_docs, n_tok, dim, total);
+  if (ws_bytes < need)
+    return fail(HPR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu < %zu bytes", ws_bytes, need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Carver c(ws);
+  float* S = c.take<float>((size_t)nq * n_docs * sizeof(float));
+  float* G = c.take<float>((size_t)nq * n_docs * sizeof(float));
+  uint16_t* amax = c.take<uint16_t>((size_t)n_docs * nq * lq * sizeof(uint16_t));
+  int64_t* part = c.take<int64_t>(part_bytes(n_docs));
+  const int n_ctrl = kLossCtrlWords;
+  int32_t* ctrl = c.take<int32_t>((size_t)n_ctrl * sizeof(int32_t));
+  float* terms = c.take<float>((size_t)nq * sizeof(float));
+  float* gq_part = c.take<float>((size_t)grad_q_ranges(n_docs, n_tok, (int64_t)nq * lq, dim) *
+                                 (size_t)nq * lq * dim * sizeof(float));
+  st = run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, S, amax, ctrl, n_ctrl, part, s);
+  if (st != HPR_OK) return st;
+  const float w = total ? 0.5f : 1.0f;
+  hipError_t e = timed("infonce", s, [&] {
+    return launch_infonce(S, nq, n_docs, pos_idx, logit_scale, w, G, terms, total ? loss + 1 : loss,
+                          scores, ctrl, s);
+  });
+  if (e != hipSuccess) return hip_fail(e, "infonce launch");
+  float* dqc = nullptr;
+  float* ddc = nullptr;
+  if (total) {
+    float* Pq = c.take<float>((size_t)nq * dim * sizeof(float));
+    float* Pd = c.take<float>((size_t)n_docs * dim * sizeof(float));
+    float* nrm_q = c.take<float>((size_t)nq * sizeof(float));
+    float* nrm_d = c.take<float>((size_t)n_docs * sizeof(float));
+    float* dC = c.take<float>((size_t)nq * n_docs * sizeof(float));
+    float* terms_c = c.take<float>((size_t)nq * sizeof(float));
+    dqc = c.take<float>((size_t)nq * dim * sizeof(float));
+    ddc = c.take<float>((size_t)n_docs * dim * sizeof(float));
+    e = timed("pool", s, [&] {
+      return launch_pool(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, Pq, Pd, nrm_q, nrm_d, s);
+    });
+    if (e != hipSuccess) return hip_fail(e, "pooling launch");
+    e = timed("contrastive", s, [&] {
+      return launch_contrastive(Pq, nrm_q, Pd, nrm_d, d_off, nq, lq, n_docs, n_tok, dim, pos_idx,
+                                tau, w, w, dC, terms_c, dqc, ddc, loss, ctrl, s);
+    });
+    if (e != hipSuccess) return hip_fail(e, "contrastive launch");
+  }
+  // With both gradients, the last step of dQ (the sum over its document ranges, plus the
+  // contrastive part) rides in the dD launch, saving a kernel launch.
+  const bool fold = dq && dd;
+  if (dq) {
+    e = timed("grad_q", s, [&] {
+      return launch_grad_q(d_tok, d_off, n_docs, n_tok, dim, nq, lq, amax, G, gq_part, dq, fold,
+                           dqc, s);
+    });
+    if (e != hipSuccess) return hip_fail(e, "dQ launch");
+  }
+  if (dd) {
+    e = timed("grad_d", s, [&] {
+      return launch_grad_d(q, d_off, n_docs, n_tok, dim, nq, lq, amax, G, dd,
+                           fold ? gq_part : nullptr, dq, fold ? dqc : nullptr, ddc, s);
+    });
+    if (e != hipSuccess) return hip_fail(e, "dD launch");
+  }
+  return HPR_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -173,15 +275,12 @@ size_t maxsim_topk_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int64_
 
 size_t coltrast_loss_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int64_t n_tok,
                                     int32_t dim) {
-  (void)n_tok, (void)dim;
-  if (nq < 1 || lq < 1 || n_docs < 1) return 0;
-  const size_t sd = align_up((size_t)nq * (size_t)n_docs * sizeof(float));
-  const size_t am = align_up((size_t)n_docs * (size_t)nq * (size_t)lq * sizeof(uint16_t));
-  const int64_t E = (int64_t)nq * lq;
-  const size_t gq = align_up((size_t)grad_q_ranges(n_docs, n_tok, E, dim) * (size_t)E *
-                             (size_t)dim * sizeof(float));
-  return 2 * sd + am + part_bytes(n_docs) + align_up((size_t)kLossCtrlWords * sizeof(int32_t)) +
-         align_up((size_t)nq * sizeof(float)) + gq;
+  return loss_ws_bytes(nq, lq, n_docs, n_tok, dim, false);
+}
+
+size_t coltrast_total_loss_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int64_t n_tok,
+                                          int32_t dim) {
+  return loss_ws_bytes(nq, lq, n_docs, n_tok, dim, true);
 }
 
 hpr_status maxsim_score(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d_tok,
@@ -233,54 +332,20 @@ hpr_status coltrast_loss_fwd_bwd(const uint16_t* q, int32_t nq, int32_t lq,
                                  int64_t n_tok, int32_t dim, const int32_t* pos_idx,
                                  float logit_scale, float* loss, float* dq, float* dd,
                                  float* scores, void* ws, size_t ws_bytes, void* stream) {
-  hpr_status st = check_maxsim_args(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim);
-  if (st == HPR_OK) st = check_lq(lq, dim, true);
-  if (st != HPR_OK) return st;
-  if (!pos_idx || !loss || !ws) return fail(HPR_ERR_INVALID_ARG, "pos_idx, loss and ws must be non-NULL");
-  if (!(logit_scale == logit_scale) || logit_scale > 3.0e38f || logit_scale < -3.0e38f)
-    return fail(HPR_ERR_INVALID_ARG, "logit_scale must be finite");
-  if ((int64_t)nq * lq > 16384)
-    return fail(HPR_ERR_UNSUPPORTED_SHAPE, "nq * lq = %lld exceeds 16384", (long long)nq * lq);
-  if ((dq && !aligned16(dq)) || (dd && !aligned16(dd)))
-    return fail(HPR_ERR_INVALID_ARG, "gradient outputs must be 16-byte aligned");
-  const size_t need = coltrast_loss_workspace_size(nq, lq, n_docs, n_tok, dim);
-  if (ws_bytes < need)
-    return fail(HPR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu < %zu bytes", ws_bytes, need);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  Carver c(ws);
-  float* S = c.take<float>((size_t)nq * n_docs * sizeof(float));
-  float* G = c.take<float>((size_t)nq * n_docs * sizeof(float));
-  uint16_t* amax = c.take<uint16_t>((size_t)n_docs * nq * lq * sizeof(uint16_t));
-  int64_t* part = c.take<int64_t>(part_bytes(n_docs));
-  const int n_ctrl = kLossCtrlWords;
-  int32_t* ctrl = c.take<int32_t>((size_t)n_ctrl * sizeof(int32_t));
-  float* terms = c.take<float>((size_t)nq * sizeof(float));
-  float* gq_part = c.take<float>((size_t)grad_q_ranges(n_docs, n_tok, (int64_t)nq * lq, dim) *
-                                 (size_t)nq * lq * dim * sizeof(float));
-  st = run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, S, amax, ctrl, n_ctrl, part, s);
-  if (st != HPR_OK) return st;
-  hipError_t e = timed("infonce", s, [&] {
-    return launch_infonce(S, nq, n_docs, pos_idx, logit_scale, G, terms, loss, scores, ctrl, s);
-  });
-  if (e != hipSuccess) return hip_fail(e, "infonce launch");
-  // With both gradients, the last step of dQ (the sum over its document ranges) rides in the
-  // dD launch, saving a kernel launch.
-  const bool fold = dq && dd;
-  if (dq) {
-    e = timed("grad_q", s, [&] {
-      return launch_grad_q(d_tok, d_off, n_docs, n_tok, dim, nq, lq, amax, G, gq_part, dq, fold,
-                           s);
-    });
-    if (e != hipSuccess) return hip_fail(e, "dQ launch");
-  }
-  if (dd) {
-    e = timed("grad_d", s, [&] {
-      return launch_grad_d(q, d_off, n_docs, n_tok, dim, nq, lq, amax, G, dd,
-                           fold ? gq_part : nullptr, dq, s);
-    });
-    if (e != hipSuccess) return hip_fail(e, "dD launch");
-  }
-  return HPR_OK;
+  return run_loss(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, pos_idx, logit_scale, 0.f, loss,
+                  dq, dd, scores, ws, ws_bytes, stream);
+}
+
+hpr_status coltrast_total_loss_fwd_bwd(const uint16_t* q, int32_t nq, int32_t lq,
+                                       const uint16_t* d_tok, const int64_t* d_off,
+                                       int64_t n_docs, int64_t n_tok, int32_t dim,
+                                       const int32_t* pos_idx, float logit_scale,
+                                       float temperature, float* loss, float* dq, float* dd,
+                                       void* ws, size_t ws_bytes, void* stream) {
+  if (!(temperature > 0.f) || temperature > 3.0e38f || !(1.0f / temperature < 3.0e38f))
+    return fail(HPR_ERR_INVALID_ARG, "temperature must be positive, finite, with finite inverse");
+  return run_loss(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, pos_idx, logit_scale, temperature,
+                  loss, dq, dd, nullptr, ws, ws_bytes, stream);
 }
 
 size_t dense_ip_topk_workspace_size(int32_t nq, int64_t n, int32_t dim, int32_t k) {

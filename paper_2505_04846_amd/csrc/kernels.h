@@ -54,22 +54,42 @@ hipError_t launch_topk_rows(const float* scores, int64_t rows, int64_t n, int64_
 // of the scores.  ctrl[0] != 0 (raised earlier) or an out-of-range positive makes the loss NaN;
 // ctrl[1] is a completion counter that must be 0 on entry (it is 0 again on exit); terms is
 // scratch of nq floats.
+// G is multiplied by gw (the loss's weight when it is one term of a weighted sum); *loss is the
+// unweighted mean.
 hipError_t launch_infonce(const float* S, int nq, int64_t n_docs, const int32_t* pos,
-                          float scale, float* G, float* terms, float* loss, float* scores_out,
-                          int32_t* ctrl, hipStream_t stream);
+                          float scale, float gw, float* G, float* terms, float* loss,
+                          float* scores_out, int32_t* ctrl, hipStream_t stream);
 
 // dQ over `grad_q_ranges` document ranges; part holds grad_q_ranges(...) * nq * lq * dim
-// floats of partial sums.  With defer_sum the sum over the ranges is left to launch_grad_d
-// (which must then be given part and dq).
+// floats of partial sums.  dqc (optional, [nq][dim]) is added to every token row of its query.
+// With defer_sum the sum over the ranges is left to launch_grad_d (which must then be given
+// part, dq and the same dqc).
 int grad_q_ranges(int64_t n_docs, int64_t n_tok, int64_t E, int dim);
 hipError_t launch_grad_q(const uint16_t* d_tok, const int64_t* off, int64_t n_docs, int64_t n_tok,
                          int dim, int nq, int lq, const uint16_t* amax, const float* G,
-                         float* part, float* dq, bool defer_sum, hipStream_t stream);
+                         float* part, float* dq, bool defer_sum, const float* dqc,
+                         hipStream_t stream);
 
-// dD; when dq_part is non-null it also finishes a deferred dQ (sums dq_part's ranges into dq).
+// dD; when dq_part is non-null it also finishes a deferred dQ (sums dq_part's ranges into dq,
+// adding dqc); ddc (optional, [n_docs][dim]) is added to every token row of its document.
 hipError_t launch_grad_d(const uint16_t* q, const int64_t* off, int64_t n_docs, int64_t n_tok,
                          int dim, int nq, int lq, const uint16_t* amax, const float* G, float* dd,
-                         const float* dq_part, float* dq, hipStream_t stream);
+                         const float* dq_part, float* dq, const float* dqc, const float* ddc,
+                         hipStream_t stream);
+
+// Pooled contrastive loss (contrastive.hip): mean-pooled rows and their norms, then the loss
+// term per query, dC = w_c dL_C/dc [nq][n_docs], the per-query and per-document gradient parts
+// dqc [nq][dim] and ddc [n_docs][dim] (weighted by w_c), and loss[2] = L_C,
+// loss[0] = w_li loss[1] + w_c loss[2] (loss[1] written earlier by launch_infonce).
+hipError_t launch_pool(const uint16_t* q, int nq, int lq, const uint16_t* d_tok,
+                       const int64_t* off, int64_t n_docs, int64_t n_tok, int dim, float* Pq,
+                       float* Pd, float* nrm_q, float* nrm_d, hipStream_t stream);
+hipError_t launch_contrastive(const float* Pq, const float* nrm_q, const float* Pd,
+                              const float* nrm_d, const int64_t* off, int nq, int lq,
+                              int64_t n_docs, int64_t n_tok, int dim, const int32_t* pos,
+                              float tau, float w_li, float w_c, float* dC, float* terms,
+                              float* dqc, float* ddc, float* loss, int32_t* ctrl,
+                              hipStream_t stream);
 
 hipError_t launch_scale(float* x, int64_t n, const float* scale, hipStream_t stream);
 

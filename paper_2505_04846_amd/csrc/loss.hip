@@ -59,9 +59,9 @@ __device__ void block_argmax(float& M, int64_t& dM, float* redf, int64_t* redi) 
 // kernels of the call, ctrl[1] = completion counter (both zeroed at the start of the call).
 __global__ __launch_bounds__(kRowThreads) void infonce_kernel(const float* __restrict__ S, int nq,
                                                               int64_t n, const int32_t* pos,
-                                                              float s, float* G, float* terms,
-                                                              float* loss, float* scores_out,
-                                                              int32_t* ctrl) {
+                                                              float s, float gw, float* G,
+                                                              float* terms, float* loss,
+                                                              float* scores_out, int32_t* ctrl) {
   // No FMA contraction in this kernel: every logit must be the same rounded product s * S.
   // Contracted, M - s * S[pos] becomes fma(-s, S[pos], M), the rounding error of M's own
   // product (up to half an ulp of ~1e3 when s = 50) instead of exactly 0 when the positive
@@ -74,7 +74,7 @@ __global__ __launch_bounds__(kRowThreads) void infonce_kernel(const float* __res
   const int q = blockIdx.x;
   const float* Sq = S + (int64_t)q * n;
   float* Gq = G + (int64_t)q * n;
-  const float gscale = s / (float)nq;
+  const float gscale = gw * s / (float)nq;  // gw: the loss's weight in a weighted sum
 
   float M = -__builtin_huge_valf();
   int64_t dM = n;
@@ -149,7 +149,7 @@ __global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
     const uint16_t* __restrict__ D, const int64_t* __restrict__ off, int64_t n_docs,
     int64_t n_tok, int dim, int nq, int lq, const uint16_t* __restrict__ amax,
     const float* __restrict__ G, float* __restrict__ part, float* __restrict__ dq, int n_groups,
-    int R) {
+    int R, bool direct) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t lin = xcd_linear(blockIdx.x, (int64_t)n_groups * R);
   const int r = (int)(lin / n_groups);
@@ -222,7 +222,7 @@ __global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
     }
   }
   if (!active) return;
-  float* dst = (R == 1 ? dq : part + (int64_t)r * E * dim) + e * dim;  // one range: final sums
+  float* dst = (direct ? dq : part + (int64_t)r * E * dim) + e * dim;  // direct: final sums
 #pragma unroll
   for (int cc = 0; cc < CPL; ++cc) {
     const int k = 8 * (c + 16 * cc);
@@ -236,12 +236,21 @@ __global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
 // dQ, second pass: dq[i] = sum over ranges r = 0, 1, ... of part[r][i], 4 values at a time.
 // Run by its own kernel, or folded into the first lines of grad_d_kernel (the next launch of the
 // call), whose workgroups each take one slice of the values.
+// dqc (optional, [nq][dim]): a per-query term added to every token's row (the contrastive part
+// of the total loss).
 __device__ __forceinline__ void grad_q_sum_ranges(const float* __restrict__ part, int R,
                                                   int64_t i0, int64_t i1, int64_t n4,
-                                                  float* __restrict__ dq) {
+                                                  float* __restrict__ dq,
+                                                  const float* __restrict__ dqc, int lq,
+                                                  int dim) {
   const f32x4* p = reinterpret_cast<const f32x4*>(part);
   for (int64_t i = i0 + threadIdx.x; i < i1; i += blockDim.x) {
     f32x4 s = p[i];
+    if (dqc) {
+      const int64_t e = 4 * i / dim;
+      const int64_t k = 4 * i - e * dim;
+      s += *reinterpret_cast<const f32x4*>(dqc + (e / lq) * dim + k);
+    }
     int r = 1;
     for (; r + 8 <= R; r += 8) {  // eight ranges' loads in flight, then added in range order
       f32x4 v[8];
@@ -256,10 +265,11 @@ __device__ __forceinline__ void grad_q_sum_ranges(const float* __restrict__ part
 }
 
 __global__ void grad_q_reduce_kernel(const float* __restrict__ part, int R, int64_t n4,
-                                     float* __restrict__ dq) {
+                                     float* __restrict__ dq, const float* __restrict__ dqc,
+                                     int lq, int dim) {
   const int64_t i0 = (int64_t)blockIdx.x * blockDim.x;
   const int64_t i1 = i0 + blockDim.x < n4 ? i0 + blockDim.x : n4;
-  grad_q_sum_ranges(part, R, i0, i1, n4, dq);
+  grad_q_sum_ranges(part, R, i0, i1, n4, dq, dqc, lq, dim);
 }
 
 constexpr int kGdWaves = 16;
@@ -303,14 +313,15 @@ __global__ __launch_bounds__(kGdThreads) void grad_d_kernel(
     const uint16_t* __restrict__ Q, const int64_t* __restrict__ off, int64_t n_docs,
     int64_t n_tok, int dim, int nq, int lq, uint64_t lq_magic,
     const uint16_t* __restrict__ amax, const float* __restrict__ G, float* __restrict__ dd,
-    const float* __restrict__ dq_part, int dq_R, float* __restrict__ dq) {
+    const float* __restrict__ dq_part, int dq_R, float* __restrict__ dq,
+    const float* __restrict__ dqc, const float* __restrict__ ddc) {
   extern __shared__ __attribute__((aligned(16))) unsigned char gd_smem[];
   constexpr int RPP = kGdThreads / TPR;
   if (dq_part) {  // the dQ range sums, one slice per workgroup (independent of the rest)
     const int64_t n4 = (int64_t)nq * lq * dim / 4;
     const int64_t per = (n4 + gridDim.x - 1) / gridDim.x;
     const int64_t i0 = per * blockIdx.x;
-    grad_q_sum_ranges(dq_part, dq_R, i0, i0 + per < n4 ? i0 + per : n4, n4, dq);
+    grad_q_sum_ranges(dq_part, dq_R, i0, i0 + per < n4 ? i0 + per : n4, n4, dq, dqc, lq, dim);
   }
   const int E = nq * lq;
   const GdLds L = gd_lds(E, nq, RPP);  // the same layout the launcher sized for this TPR
@@ -451,10 +462,14 @@ __global__ __launch_bounds__(kGdThreads) void grad_d_kernel(
       for (int i = 0; i < 4; ++i) {
         const int c = cp + TPR * i;
         if (8 * c < dim) {
-          *reinterpret_cast<f32x4*>(drow + 8 * c) =
-              f32x4{acc[8 * i], acc[8 * i + 1], acc[8 * i + 2], acc[8 * i + 3]};
-          *reinterpret_cast<f32x4*>(drow + 8 * c + 4) =
-              f32x4{acc[8 * i + 4], acc[8 * i + 5], acc[8 * i + 6], acc[8 * i + 7]};
+          f32x4 v0 = f32x4{acc[8 * i], acc[8 * i + 1], acc[8 * i + 2], acc[8 * i + 3]};
+          f32x4 v1 = f32x4{acc[8 * i + 4], acc[8 * i + 5], acc[8 * i + 6], acc[8 * i + 7]};
+          if (ddc) {  // the document's contrastive part, the same for each of its rows
+            v0 += *reinterpret_cast<const f32x4*>(ddc + d * dim + 8 * c);
+            v1 += *reinterpret_cast<const f32x4*>(ddc + d * dim + 8 * c + 4);
+          }
+          *reinterpret_cast<f32x4*>(drow + 8 * c) = v0;
+          *reinterpret_cast<f32x4*>(drow + 8 * c + 4) = v1;
         }
       }
     }
@@ -472,10 +487,10 @@ __global__ void scale_kernel(float* x, int64_t n, const float* scale) {
 }  // namespace
 
 hipError_t launch_infonce(const float* S, int nq, int64_t n_docs, const int32_t* pos, float scale,
-                          float* G, float* terms, float* loss, float* scores_out, int32_t* ctrl,
-                          hipStream_t stream) {
+                          float gw, float* G, float* terms, float* loss, float* scores_out,
+                          int32_t* ctrl, hipStream_t stream) {
   hipLaunchKernelGGL(infonce_kernel, dim3((unsigned)nq), dim3(kRowThreads), 0, stream, S, nq,
-                     n_docs, pos, scale, G, terms, loss, scores_out, ctrl);
+                     n_docs, pos, scale, gw, G, terms, loss, scores_out, ctrl);
   return hipGetLastError();
 }
 
@@ -492,21 +507,23 @@ int grad_q_ranges(int64_t n_docs, int64_t n_tok, int64_t E, int dim) {
 
 hipError_t launch_grad_q(const uint16_t* d_tok, const int64_t* off, int64_t n_docs, int64_t n_tok,
                          int dim, int nq, int lq, const uint16_t* amax, const float* G,
-                         float* part, float* dq, bool defer_sum, hipStream_t stream) {
+                         float* part, float* dq, bool defer_sum, const float* dqc,
+                         hipStream_t stream) {
   const int64_t E = (int64_t)nq * lq;
   const int R = grad_q_ranges(n_docs, n_tok, E, dim);
   const int n_groups = (int)((E + kGqEntries - 1) / kGqEntries);
   const unsigned blocks = (unsigned)((int64_t)n_groups * R);
+  const bool direct = R == 1 && !dqc;  // one range and nothing to add: write the final sums
   if (dim <= 128)
     hipLaunchKernelGGL(grad_q_part_kernel<1>, dim3(blocks), dim3(kGqThreads), 0, stream, d_tok,
-                       off, n_docs, n_tok, dim, nq, lq, amax, G, part, dq, n_groups, R);
+                       off, n_docs, n_tok, dim, nq, lq, amax, G, part, dq, n_groups, R, direct);
   else
     hipLaunchKernelGGL(grad_q_part_kernel<2>, dim3(blocks), dim3(kGqThreads), 0, stream, d_tok,
-                       off, n_docs, n_tok, dim, nq, lq, amax, G, part, dq, n_groups, R);
-  if (R > 1 && !defer_sum) {
+                       off, n_docs, n_tok, dim, nq, lq, amax, G, part, dq, n_groups, R, direct);
+  if (!direct && !defer_sum) {
     const int64_t n4 = E * dim / 4;
     hipLaunchKernelGGL(grad_q_reduce_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0,
-                       stream, part, R, n4, dq);
+                       stream, part, R, n4, dq, dqc, lq, dim);
   }
   return hipGetLastError();
 }
@@ -515,7 +532,7 @@ template <int TPR>
 hipError_t launch_grad_d_t(const uint16_t* q, const int64_t* off, int64_t n_docs, int64_t n_tok,
                            int dim, int nq, int lq, uint64_t magic, const uint16_t* amax,
                            const float* G, float* dd, const float* dq_part, int dq_R, float* dq,
-                           hipStream_t stream) {
+                           const float* dqc, const float* ddc, hipStream_t stream) {
   const int lds = gd_lds(nq * lq, nq, kGdThreads / TPR).total;
   if (lds > 65536) {  // beyond the default dynamic LDS limit (large nq * lq only)
     const hipError_t e = hipFuncSetAttribute((const void*)grad_d_kernel<TPR>,
@@ -523,22 +540,24 @@ hipError_t launch_grad_d_t(const uint16_t* q, const int64_t* off, int64_t n_docs
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(grad_d_kernel<TPR>, dim3((unsigned)n_docs), dim3(kGdThreads), lds, stream, q,
-                     off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq);
+                     off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, dqc,
+                     ddc);
   return hipGetLastError();
 }
 
 hipError_t launch_grad_d(const uint16_t* q, const int64_t* off, int64_t n_docs, int64_t n_tok,
                          int dim, int nq, int lq, const uint16_t* amax, const float* G, float* dd,
-                         const float* dq_part, float* dq, hipStream_t stream) {
+                         const float* dq_part, float* dq, const float* dqc, const float* ddc,
+                         hipStream_t stream) {
   const int dq_R = dq_part ? grad_q_ranges(n_docs, n_tok, (int64_t)nq * lq, dim) : 0;
-  if (dq_R <= 1) dq_part = nullptr;  // one range: grad_q wrote the final sums
+  if (dq_R <= 1 && !dqc) dq_part = nullptr;  // one range, nothing to add: grad_q wrote dq
   // floor(e / lq) = (e * ceil(2^32 / lq)) >> 32 for e < 2^14 and lq <= 128: the product
   // overshoots e / lq by less than e / 2^32 < 2^-18, below the 1 / lq gap to the next integer.
   const uint64_t magic = (0x100000000ull + (uint64_t)lq - 1) / (uint64_t)lq;
   switch (gd_tpr(dim)) {
-    case 2: return launch_grad_d_t<2>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, stream);
-    case 4: return launch_grad_d_t<4>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, stream);
-    case 8: return launch_grad_d_t<8>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, stream);
+    case 2: return launch_grad_d_t<2>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, dqc, ddc, stream);
+    case 4: return launch_grad_d_t<4>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, dqc, ddc, stream);
+    case 8: return launch_grad_d_t<8>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, dqc, ddc, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -95,6 +95,38 @@ def test_loss_rejects(kw, status):
     assert _loss(**kw) == status
 
 
+def _total(**kw):
+    a = dict(q=FAKE, nq=4, lq=32, d=FAKE, off=FAKE, n_docs=8, n_tok=256, dim=128, pos=FAKE,
+             scale=50.0, tau=0.05, loss=FAKE, dq=FAKE, dd=FAKE, ws=FAKE, ws_bytes=BIG)
+    a.update(kw)
+    return hpr.lib().coltrast_total_loss_fwd_bwd(
+        a["q"], a["nq"], a["lq"], a["d"], a["off"], a["n_docs"], a["n_tok"], a["dim"], a["pos"],
+        a["scale"], a["tau"], a["loss"], a["dq"], a["dd"], a["ws"], a["ws_bytes"], NULL)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(pos=NULL), 1), (dict(loss=NULL), 1), (dict(ws=NULL), 1), (dict(q=NULL), 1),
+    (dict(scale=float("nan")), 1), (dict(tau=0.0), 1), (dict(tau=-0.05), 1),
+    (dict(tau=float("nan")), 1), (dict(tau=float("inf")), 1), (dict(tau=1e-40), 1),
+    (dict(nq=1024, lq=32), 4), (dict(dd=FAKE_ODD), 1), (dict(lq=65), 4), (dict(dim=12), 4),
+    (dict(ws_bytes=100), 5),
+])
+def test_total_loss_rejects(kw, status):
+    assert _total(**kw) == status
+    assert hpr.lib().hpr_last_error()
+
+
+def test_total_loss_workspace_holds_the_li_workspace():
+    lib = hpr.lib()
+    li = lib.coltrast_loss_workspace_size(64, 32, 512, 131072, 128)
+    tot = lib.coltrast_total_loss_workspace_size(64, 32, 512, 131072, 128)
+    # plus pooled rows, norms, dL_C/dc, terms and the gradient parts
+    extra = 4 * (2 * 64 * 128 + 2 * 512 * 128 + 2 * 64 + 512 + 64 * 512)
+    assert tot >= li + extra and tot % 256 == 0
+    assert _total(ws_bytes=tot - 1, nq=64, n_docs=512, n_tok=131072) == 5
+    assert lib.coltrast_total_loss_workspace_size(0, 32, 512, 131072, 128) == 0
+
+
 def test_workspace_sizes_are_consistent():
     lib = hpr.lib()
     s1 = lib.maxsim_score_workspace_size(64, 32, 512, 131072, 128)

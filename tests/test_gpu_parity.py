@@ -309,7 +309,7 @@ def test_autograd_function_matches_fwd_bwd_and_scales():
     ref = hpr.coltrast_loss_fwd_bwd(Q.detach(), D.detach(), off, pos, 1.5625)
     assert torch.allclose(Q.grad.float(), (3.0 * ref["dq"]).bfloat16().float())
     assert torch.allclose(D.grad.float(), (3.0 * ref["dd"]).bfloat16().float())
-    assert float(loss) == float(ref["loss"][0])
+    assert float(loss.detach()) == float(ref["loss"][0])
 
 
 # ------------------------------------------------------------------------------ plumbing

@@ -1,0 +1,186 @@
+"""GPU parity of the whole ColTrast loss L = (L_LI + L_C) / 2 (coltrast_total_loss_fwd_bwd)
+against the fp64 oracle (oracle.coltrast_total_loss), through the C ABI.
+
+Tolerances: the three losses within relative 2e-3 (the bar for scores and loss); gradients
+within relative L2 error 2e-3 per tensor; where the L_LI half of a document row is zero (no
+query token selects the row) the row is half of L_C's gradient alone, checked element by
+element within 2e-3 of the row's largest entry.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2505_04846_amd as hpr
+import synth
+
+pytestmark = pytest.mark.gpu
+
+REL = 2e-3
+DEV = "cuda:0"
+
+
+def _bf(t):
+    return oracle.decode_bf16(t.detach().cpu().contiguous().view(torch.int16).numpy())
+
+
+def _ragged(seed, nq, lq, lens, dim):
+    g = torch.Generator().manual_seed(seed)
+    lens = torch.tensor(lens, dtype=torch.int64)
+    off = synth.csr_offsets(lens)
+    Q = synth.unit_rows(nq * lq, dim, g, "cpu", torch.bfloat16).reshape(nq, lq, dim)
+    D = synth.unit_rows(int(off[-1]), dim, g, "cpu", torch.bfloat16)
+    return Q, D, off
+
+
+def _to_dev(*ts):
+    return [t.to(DEV) for t in ts]
+
+
+def _rel_l2(g, o):
+    g = np.asarray(g, dtype=np.float64)
+    o = np.asarray(o, dtype=np.float64)
+    return float(np.linalg.norm(g - o) / max(np.linalg.norm(o), 1e-300))
+
+
+def _parity(Q, D, off, pos, scale, tau):
+    r = hpr.coltrast_total_loss_fwd_bwd(*_to_dev(Q, D, off, pos), scale, tau)
+    Qo, Do = _bf(Q), _bf(D)
+    o = oracle.coltrast_total_loss(Qo, Do, off.numpy(), pos.numpy(), scale, tau)
+    got = r["loss"].cpu().numpy().astype(np.float64)
+    for i, key in enumerate(("loss", "loss_li", "loss_c")):
+        want = o[key]
+        assert abs(got[i] - want) <= REL * max(abs(want), 1e-3), (key, got[i], want)
+    dq = r["dq"].cpu().numpy()
+    dd = r["dd"].cpu().numpy()
+    assert _rel_l2(dq, o["dQ"]) <= REL, f"dQ rel L2 {_rel_l2(dq, o['dQ']):.3g}"
+    assert _rel_l2(dd, o["dD"]) <= REL, f"dD rel L2 {_rel_l2(dd, o['dD']):.3g}"
+    # rows L_LI leaves at zero (in the oracle and in the L_LI call alike; a near-tie of two
+    # dot products may select another token in fp32) carry L_C's part alone: check them entry
+    # by entry
+    li = oracle.coltrast_li_loss(Qo, Do, off.numpy(), pos.numpy(), scale)
+    li_gpu = hpr.coltrast_loss_fwd_bwd(*_to_dev(Q, D, off, pos), scale)["dd"].cpu().numpy()
+    c = oracle.contrastive_loss(Qo, Do, off.numpy(), pos.numpy(), tau)
+    free = ~np.any(li["dD"] != 0, axis=1) & ~np.any(li_gpu != 0, axis=1)
+    if free.any():
+        want = 0.5 * c["dD"][free]
+        lim = REL * np.abs(want).max(axis=1, keepdims=True) + 1e-30
+        assert np.all(np.abs(dd[free] - want) <= lim), "L_C rows of dD"
+    return r, o
+
+
+@pytest.mark.parametrize("tau", [0.05, 1.0])
+def test_coltrast_step_total_loss_and_grads(tau):
+    w = synth.coltrast_step(seed=0)
+    _parity(w["Q"], w["D"], w["off"], w["pos"], 1.5625, tau)
+
+
+@pytest.mark.parametrize("nq,lq,lens,dim,scale,tau", [
+    (1, 1, [1], 8, 1.0, 0.05),                     # one document: L_C = 0, its gradient 0
+    (1, 1, [1, 1], 8, 1.0, 0.5),
+    (3, 5, [4, 9, 1, 17], 16, 2.0, 0.05),
+    (4, 17, [33, 16, 5, 70, 8], 64, 0.7, 0.2),
+    (6, 32, [100, 1, 47, 256, 300, 12, 64], 128, 10.0, 0.05),
+    (5, 12, [40, 300, 7, 90, 2, 18], 120, 3.0, 0.1),  # dim not a power of two
+    (2, 32, [20, 21, 22], 256, 3.0, 0.05),
+    (3, 64, [70, 5, 33], 128, 2.0, 0.05),
+    (9, 8, [3] * 700, 32, 1.0, 0.05),              # more documents than a workgroup's threads
+])
+def test_total_loss_small_shapes(nq, lq, lens, dim, scale, tau):
+    Q, D, off = _ragged(nq * 11 + lq, nq, lq, lens, dim)
+    g = torch.Generator().manual_seed(nq + 100)
+    pos = torch.randint(0, len(lens), (nq,), generator=g, dtype=torch.int32)
+    _parity(Q, D, off, pos, scale, tau)
+
+
+def test_total_loss_dominant_positive_keeps_small_loss_accurate():
+    # every query's positive holds the query's own tokens: cosine 1 against < 0.25 for the
+    # others, so with tau = 0.04 each L_C term is ~ exp(-19), far below fp32's epsilon: the
+    # loss must stay accurate (log1p of the small sum), not 0 or a rounding residue of the
+    # log-sum-exp.  (fp64 still resolves 1 + exp(-19), so the oracle's plain log-sum-exp is
+    # accurate to ~1e-8 relative here.)
+    nq, lq, dim = 4, 8, 64
+    Q, D, off = _ragged(77, nq, lq, [lq] * nq + [30, 30], dim)
+    D = D.clone()
+    for q in range(nq):
+        D[q * lq:(q + 1) * lq] = Q[q]
+    pos = torch.arange(nq, dtype=torch.int32)
+    r = hpr.coltrast_total_loss_fwd_bwd(*_to_dev(Q, D, off, pos), 1.0, 0.04)
+    c = oracle.contrastive_loss(_bf(Q), _bf(D), off.numpy(), pos.numpy(), 0.04)
+    got = float(r["loss"][2])
+    assert 1e-12 < c["loss"] < 1e-7
+    assert abs(got - c["loss"]) <= 1e-3 * c["loss"], (got, c["loss"])
+
+
+def test_total_loss_grads_optional_and_deterministic():
+    w = synth.coltrast_step(seed=1, nq=8, n_neg=3, ld=64)
+    args = _to_dev(w["Q"], w["D"], w["off"], w["pos"])
+    full = hpr.coltrast_total_loss_fwd_bwd(*args, 1.5625, 0.05)
+    again = hpr.coltrast_total_loss_fwd_bwd(*args, 1.5625, 0.05)
+    for key in ("loss", "dq", "dd"):
+        assert torch.equal(full[key], again[key]), f"{key} not bit-reproducible"
+    only_q = hpr.coltrast_total_loss_fwd_bwd(*args, 1.5625, 0.05, need_dd=False)
+    only_d = hpr.coltrast_total_loss_fwd_bwd(*args, 1.5625, 0.05, need_dq=False)
+    assert only_q["dd"] is None and only_d["dq"] is None
+    # dQ alone takes the separate range-sum kernel; same sums in the same order
+    assert torch.equal(only_q["dq"], full["dq"]) and torch.equal(only_d["dd"], full["dd"])
+    assert torch.equal(only_q["loss"], full["loss"])
+    # the L_LI half is the L_LI call's loss
+    li = hpr.coltrast_loss_fwd_bwd(*args, 1.5625)
+    assert float(full["loss"][1]) == float(li["loss"][0])
+
+
+def test_total_loss_bad_positive_gives_nan():
+    w = synth.coltrast_step(seed=2, nq=4, n_neg=1, ld=32)
+    pos = w["pos"].clone()
+    pos[2] = -1
+    r = hpr.coltrast_total_loss_fwd_bwd(*_to_dev(w["Q"], w["D"], w["off"], pos), 1.0, 0.05)
+    assert all(math.isnan(v) for v in r["loss"].cpu().tolist())
+    # a later valid call on the same workspace is unaffected
+    ws = hpr.coltrast_total_workspace(*_to_dev(w["Q"], w["D"], w["off"]))
+    args = _to_dev(w["Q"], w["D"], w["off"])
+    bad = hpr.coltrast_total_loss_fwd_bwd(*args, pos.to(DEV), 1.0, 0.05, ws=ws)
+    good = hpr.coltrast_total_loss_fwd_bwd(*args, w["pos"].to(DEV), 1.0, 0.05, ws=ws)
+    assert math.isnan(float(bad["loss"][0]))
+    assert not any(math.isnan(v) for v in good["loss"].cpu().tolist())
+
+
+def test_total_autograd_matches_fwd_bwd_and_scales():
+    w = synth.coltrast_step(seed=3, nq=4, n_neg=3, ld=32)
+    Q = w["Q"].to(DEV).requires_grad_(True)
+    D = w["D"].to(DEV).requires_grad_(True)
+    off, pos = _to_dev(w["off"], w["pos"])
+    loss = hpr.coltrast_total_loss(Q, D, off, pos, 1.5625, 0.05)
+    (2.5 * loss).backward()
+    ref = hpr.coltrast_total_loss_fwd_bwd(Q.detach(), D.detach(), off, pos, 1.5625, 0.05)
+    assert torch.allclose(Q.grad.float(), (2.5 * ref["dq"]).bfloat16().float())
+    assert torch.allclose(D.grad.float(), (2.5 * ref["dd"]).bfloat16().float())
+    assert float(loss.detach()) == float(ref["loss"][0])
+
+
+def test_total_loss_call_replays_correctly_in_a_hip_graph():
+    w = synth.coltrast_step(seed=5, nq=16, n_neg=7, ld=64)
+    Q, D, off, pos = _to_dev(w["Q"], w["D"], w["off"], w["pos"])
+    ws = hpr.coltrast_total_workspace(Q, D, off)
+    out = {"loss": torch.empty(3, device=DEV), "dq": torch.empty(Q.shape, device=DEV),
+           "dd": torch.empty(D.shape, device=DEV)}
+    eager = hpr.coltrast_total_loss_fwd_bwd(Q, D, off, pos, 1.5625, 0.05)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        hpr.coltrast_total_loss_fwd_bwd(Q, D, off, pos, 1.5625, 0.05, ws=ws, out=out)
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        hpr.coltrast_total_loss_fwd_bwd(Q, D, off, pos, 1.5625, 0.05, ws=ws, out=out)
+    for rep in range(4):
+        for key in ("loss", "dq", "dd"):
+            out[key].fill_(float("nan"))
+        g.replay()
+        hpr.maxsim_score(Q, D, off)             # unrelated eager work between replays
+        torch.cuda.synchronize()
+        for key in ("loss", "dq", "dd"):
+            assert torch.equal(out[key], eager[key]), f"replay {rep}: {key} differs"
