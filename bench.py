@@ -5,7 +5,9 @@
 Default workload: the ColTrast training step (64 queries x 32 tokens against 512 in-batch
 documents x 256 tokens, dim 128, bf16): one step = one coltrast_loss_fwd_bwd call, i.e. CSR
 partition, MaxSim scoring with the fused max/argmax, InfoNCE loss, and the dQ and dD
-gradients.  Other workloads (--workload): li_retrieval (1,024 x 32 queries against 500,000
+gradients.  Other workloads (--workload): coltrast_total (the same batch under the whole
+ColTrast loss (L_LI + L_C) / 2, adding mean pooling and the pooled-cosine contrastive loss),
+li_retrieval (1,024 x 32 queries against 500,000
 ragged documents, exact top-100), li_large (4,096 x 64 against 1,000,000 lognormal documents,
 top-1000), dense_retrieval (4,096 queries against 10,000,000 fp16 rows of dim 4096, top-100),
 tiny_maxsim.
@@ -33,8 +35,8 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBS = 8000.0
 COPY_CALIBRATION_BYTES = 256 << 20  # bytes read (and written) by each calibration copy
 CPU_SAMPLE_SECONDS = 10.0  # the oracle sample is repeated for at least this long
-KERNELS = ("partition", "maxsim", "maxsim_argmax", "topk", "infonce", "grad_q", "grad_d",
-           "dense_sample", "dense_scan", "dense_merge")
+KERNELS = ("partition", "maxsim", "maxsim_argmax", "topk", "infonce", "pool", "contrastive",
+           "grad_q", "grad_d", "dense_sample", "dense_scan", "dense_merge")
 
 
 def parse():
@@ -43,10 +45,13 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="coltrast_step",
-                    choices=["coltrast_step", "li_retrieval", "li_large", "dense_retrieval",
-                             "tiny_maxsim"])
+                    choices=["coltrast_step", "coltrast_total", "li_retrieval", "li_large",
+                             "dense_retrieval", "tiny_maxsim"])
     ap.add_argument("--logit-scale", type=float, default=1.5625,
-                    help="inverse temperature of the InfoNCE logits (coltrast_step)")
+                    help="inverse temperature of the InfoNCE logits over MaxSim scores "
+                         "(coltrast_step, coltrast_total)")
+    ap.add_argument("--temperature", type=float, default=0.05,
+                    help="temperature of the pooled-cosine contrastive loss (coltrast_total)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the extra HIP-graph replay timing of the same step")
@@ -88,23 +93,28 @@ def blas_threads():
     return len(os.sched_getaffinity(0))
 
 
-def build_workload(name, dev, scale):
+def build_workload(name, dev, scale, tau):
     import torch
     import paper_2505_04846_amd as hpr
     import synth
 
-    if name in ("coltrast_step",):
+    if name in ("coltrast_step", "coltrast_total"):
+        total = name == "coltrast_total"
         w = synth.coltrast_step(seed=0, device="cpu")
         Q, D, off, pos = (w[k].to(dev) for k in ("Q", "D", "off", "pos"))
         nq, lq, dim = Q.shape
         n_docs = off.numel() - 1
-        ws = hpr.coltrast_workspace(Q, D, off)
-        out = {"loss": torch.empty(1, dtype=torch.float32, device=dev),
+        ws = (hpr.coltrast_total_workspace if total else hpr.coltrast_workspace)(Q, D, off)
+        out = {"loss": torch.empty(3 if total else 1, dtype=torch.float32, device=dev),
                "dq": torch.empty(Q.shape, dtype=torch.float32, device=dev),
                "dd": torch.empty(D.shape, dtype=torch.float32, device=dev)}
 
-        def step():
-            hpr.coltrast_loss_fwd_bwd(Q, D, off, pos, scale, ws=ws, out=out)
+        if total:
+            def step():
+                hpr.coltrast_total_loss_fwd_bwd(Q, D, off, pos, scale, tau, ws=ws, out=out)
+        else:
+            def step():
+                hpr.coltrast_loss_fwd_bwd(Q, D, off, pos, scale, ws=ws, out=out)
 
         lens = (w["off"][1:] - w["off"][:-1]).to(torch.float64)
         flops = 2.0 * dim * lq * nq * float(lens.sum())
@@ -115,14 +125,20 @@ def build_workload(name, dev, scale):
             args = (bf(w["Q"]), bf(w["D"]), w["off"].numpy(), w["pos"].numpy(), scale)
             reps, t0 = 0, time.perf_counter()
             while reps == 0 or time.perf_counter() - t0 < CPU_SAMPLE_SECONDS:
-                oracle.coltrast_li_loss(*args)
+                if total:
+                    oracle.coltrast_total_loss(*args, tau)
+                else:
+                    oracle.coltrast_li_loss(*args)
                 reps += 1
             dt = time.perf_counter() - t0
             return reps * nq * n_docs / dt, (f"the full workload {reps} times: loss, dQ and dD "
                                              f"({nq} x {n_docs} pairs each)")
 
-        cfg = {"workload": "coltrast_step", "nq": nq, "lq": lq, "n_docs": n_docs, "ld": 256,
+        cfg = {"workload": name, "nq": nq, "lq": lq, "n_docs": n_docs, "ld": 256,
                "dim": dim, "hard_negatives_per_query": 7, "logit_scale": scale}
+        if total:
+            cfg.update(loss="(L_LI + L_C) / 2", contrastive_temperature=tau,
+                       pooling="mean over tokens")
         return dict(step=step, pairs=nq * n_docs, kernel="maxsim_argmax", flops=flops,
                     cpu_sample=cpu_sample, config=cfg, dtype="bf16", unit="pairs/s",
                     sha=source_sha("maxsim.hip", "common.h"), graph_primary=True)
@@ -249,7 +265,7 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    W = build_workload(args.workload, dev, args.logit_scale)
+    W = build_workload(args.workload, dev, args.logit_scale, args.temperature)
     print(f"[bench] workload {args.workload} ready", file=sys.stderr, flush=True)
 
     for _ in range(args.warmup):

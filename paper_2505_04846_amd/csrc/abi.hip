@@ -218,21 +218,21 @@ hpr_status run_loss(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d
   float* dqc = nullptr;
   float* ddc = nullptr;
   if (total) {
-    float* Pq = c.take<float>((size_t)nq * dim * sizeof(float));
-    float* Pd = c.take<float>((size_t)n_docs * dim * sizeof(float));
-    float* nrm_q = c.take<float>((size_t)nq * sizeof(float));
-    float* nrm_d = c.take<float>((size_t)n_docs * sizeof(float));
+    float* Uq = c.take<float>((size_t)nq * dim * sizeof(float));
+    float* Ud = c.take<float>((size_t)n_docs * dim * sizeof(float));
+    float* gsc_q = c.take<float>((size_t)nq * sizeof(float));
+    float* gsc_d = c.take<float>((size_t)n_docs * sizeof(float));
     float* dC = c.take<float>((size_t)nq * n_docs * sizeof(float));
     float* terms_c = c.take<float>((size_t)nq * sizeof(float));
     dqc = c.take<float>((size_t)nq * dim * sizeof(float));
     ddc = c.take<float>((size_t)n_docs * dim * sizeof(float));
     e = timed("pool", s, [&] {
-      return launch_pool(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, Pq, Pd, nrm_q, nrm_d, s);
+      return launch_pool(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, Uq, Ud, gsc_q, gsc_d, s);
     });
     if (e != hipSuccess) return hip_fail(e, "pooling launch");
     e = timed("contrastive", s, [&] {
-      return launch_contrastive(Pq, nrm_q, Pd, nrm_d, d_off, nq, lq, n_docs, n_tok, dim, pos_idx,
-                                tau, w, w, dC, terms_c, dqc, ddc, loss, ctrl, s);
+      return launch_contrastive(Uq, gsc_q, Ud, gsc_d, nq, n_docs, dim, pos_idx, tau, w, w, dC,
+                                terms_c, dqc, ddc, loss, ctrl, s);
     });
     if (e != hipSuccess) return hip_fail(e, "contrastive launch");
   }

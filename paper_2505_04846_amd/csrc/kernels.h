@@ -77,18 +77,19 @@ hipError_t launch_grad_d(const uint16_t* q, const int64_t* off, int64_t n_docs, 
                          const float* dq_part, float* dq, const float* dqc, const float* ddc,
                          hipStream_t stream);
 
-// Pooled contrastive loss (contrastive.hip): mean-pooled rows and their norms, then the loss
+// Pooled contrastive loss (contrastive.hip).  launch_pool: the unit mean-pooled rows Uq
+// [nq][dim], Ud [n_docs][dim] and the gradient scales 1 / (|P| L).  launch_contrastive: the loss
 // term per query, dC = w_c dL_C/dc [nq][n_docs], the per-query and per-document gradient parts
 // dqc [nq][dim] and ddc [n_docs][dim] (weighted by w_c), and loss[2] = L_C,
 // loss[0] = w_li loss[1] + w_c loss[2] (loss[1] written earlier by launch_infonce).
+// dim % 8 == 0, dim <= 256.
 hipError_t launch_pool(const uint16_t* q, int nq, int lq, const uint16_t* d_tok,
-                       const int64_t* off, int64_t n_docs, int64_t n_tok, int dim, float* Pq,
-                       float* Pd, float* nrm_q, float* nrm_d, hipStream_t stream);
-hipError_t launch_contrastive(const float* Pq, const float* nrm_q, const float* Pd,
-                              const float* nrm_d, const int64_t* off, int nq, int lq,
-                              int64_t n_docs, int64_t n_tok, int dim, const int32_t* pos,
-                              float tau, float w_li, float w_c, float* dC, float* terms,
-                              float* dqc, float* ddc, float* loss, int32_t* ctrl,
+                       const int64_t* off, int64_t n_docs, int64_t n_tok, int dim, float* Uq,
+                       float* Ud, float* gsc_q, float* gsc_d, hipStream_t stream);
+hipError_t launch_contrastive(const float* Uq, const float* gsc_q, const float* Ud,
+                              const float* gsc_d, int nq, int64_t n_docs, int dim,
+                              const int32_t* pos, float tau, float w_li, float w_c, float* dC,
+                              float* terms, float* dqc, float* ddc, float* loss, int32_t* ctrl,
                               hipStream_t stream);
 
 hipError_t launch_scale(float* x, int64_t n, const float* scale, hipStream_t stream);

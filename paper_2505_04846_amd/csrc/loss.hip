@@ -420,10 +420,29 @@ __global__ __launch_bounds__(kGdThreads) void grad_d_kernel(
     }
     __syncthreads();
 
-    // row j's entries, kGdBatch at a time (absent entries repeat a valid one with weight 0)
+    // row j's entries, kGdBatch at a time (absent entries repeat a valid one with weight 0),
+    // added to the document's contrastive part (the same for each of its rows) when there is one
     float acc[kGdCols];
 #pragma unroll
     for (int v = 0; v < kGdCols; ++v) acc[v] = 0.f;
+    if (ddc) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int c = cp + TPR * i;
+        if (8 * c < dim) {
+          const f32x4 v0 = *reinterpret_cast<const f32x4*>(ddc + d * dim + 8 * c);
+          const f32x4 v1 = *reinterpret_cast<const f32x4*>(ddc + d * dim + 8 * c + 4);
+          acc[8 * i + 0] = v0.x;
+          acc[8 * i + 1] = v0.y;
+          acc[8 * i + 2] = v0.z;
+          acc[8 * i + 3] = v0.w;
+          acc[8 * i + 4] = v1.x;
+          acc[8 * i + 5] = v1.y;
+          acc[8 * i + 6] = v1.z;
+          acc[8 * i + 7] = v1.w;
+        }
+      }
+    }
     if (j < Wn) {
       const int p_end = rs[j + 1];
       for (int p = rs[j]; p < p_end; p += kGdBatch) {
@@ -462,14 +481,10 @@ __global__ __launch_bounds__(kGdThreads) void grad_d_kernel(
       for (int i = 0; i < 4; ++i) {
         const int c = cp + TPR * i;
         if (8 * c < dim) {
-          f32x4 v0 = f32x4{acc[8 * i], acc[8 * i + 1], acc[8 * i + 2], acc[8 * i + 3]};
-          f32x4 v1 = f32x4{acc[8 * i + 4], acc[8 * i + 5], acc[8 * i + 6], acc[8 * i + 7]};
-          if (ddc) {  // the document's contrastive part, the same for each of its rows
-            v0 += *reinterpret_cast<const f32x4*>(ddc + d * dim + 8 * c);
-            v1 += *reinterpret_cast<const f32x4*>(ddc + d * dim + 8 * c + 4);
-          }
-          *reinterpret_cast<f32x4*>(drow + 8 * c) = v0;
-          *reinterpret_cast<f32x4*>(drow + 8 * c + 4) = v1;
+          *reinterpret_cast<f32x4*>(drow + 8 * c) =
+              f32x4{acc[8 * i], acc[8 * i + 1], acc[8 * i + 2], acc[8 * i + 3]};
+          *reinterpret_cast<f32x4*>(drow + 8 * c + 4) =
+              f32x4{acc[8 * i + 4], acc[8 * i + 5], acc[8 * i + 6], acc[8 * i + 7]};
         }
       }
     }

@@ -88,6 +88,7 @@ def test_coltrast_step_total_loss_and_grads(tau):
     (2, 32, [20, 21, 22], 256, 3.0, 0.05),
     (3, 64, [70, 5, 33], 128, 2.0, 0.05),
     (9, 8, [3] * 700, 32, 1.0, 0.05),              # more documents than a workgroup's threads
+    (3, 4, [1, 2] * 4600, 8, 1.0, 0.05),           # a row too long to stay in LDS
 ])
 def test_total_loss_small_shapes(nq, lq, lens, dim, scale, tau):
     Q, D, off = _ragged(nq * 11 + lq, nq, lq, lens, dim)
