@@ -14,9 +14,10 @@
 //   * C layout (32x32): lane l holds column l % 32 (a query slot) and the 16 rows
 //     8 (i / 4) + 4 (l / 32) + i % 4, i = 0..15 (document tokens).  The plain score folds each
 //     tile's 16 values into one running max per lane with v_max3 (8 instructions per tile and
-//     block); the argmax variant also keeps the tile of the running maximum and a copy of that
-//     tile's 16 values, from which the row is recovered at the end of the document.  There the
-//     two half-waves are combined and the slot maxima summed per query.
+//     block); in the argmax variant a tile whose maximum is strictly larger than the running one
+//     also finds the lowest of its rows holding it (the document token is kept, not the tile's
+//     values), which leaves room for three resident workgroups per CU.  At the end of a
+//     document the two half-waves are combined and the slot maxima summed per query.
 //   * Workgroup = 4 waves on 4 query sets, all consuming the same stream of document tiles,
 //     which the workgroup stages through LDS (double-buffered, one stage in flight).  Workgroups
 //     sharing a document range are mapped onto the same XCD and start together, so the range is
@@ -106,12 +107,14 @@ __device__ __forceinline__ float half32_sum(float v) {
   return v;
 }
 
-// Waves per SIMD the register allocation must allow: two (up to 256 VGPRs), which leaves the
-// dim-128 plain variant room for 128 query slots per wave (measured 7-10 % faster than 64
+// Waves per SIMD the register allocation must allow.  Plain: two (up to 256 VGPRs), which
+// leaves the dim-128 variant room for 128 query slots per wave (measured 7-10 % faster than 64
 // slots at three waves per SIMD: half the LDS operand reads per MFMA and half the query groups,
-// hence half the document-range re-reads).
+// hence half the document-range re-reads).  Argmax: three (up to 168 VGPRs) with 64 slots per
+// wave, measured 10 % faster than two; 128 slots with the per-tile row search did not fit 256
+// VGPRs without spills and was slower.
 template <int KS, bool ARGMAX>
-constexpr int maxsim_occupancy() { return 2; }
+constexpr int maxsim_occupancy() { return ARGMAX ? 3 : 2; }
 
 template <int KS, int NB, int WPW, bool ARGMAX>
 __global__ __launch_bounds__(64 * WPW, (maxsim_occupancy<KS, ARGMAX>())) void maxsim_kernel(
@@ -257,20 +260,15 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_occupancy<KS, ARGMAX>())) void ma
     }
   };
 
-  // Running state per lane and block.  Plain: rm[b][0], the maximum so far.  Argmax: rm[b][0]
-  // and the tile bt[b] holding it, plus that tile's 16 row values bv[b][:] (copied whenever a
-  // later tile's maximum is strictly larger, so the earliest tile keeps ties); the row within
-  // the tile is found once, at the end of the document.
-  constexpr int kVals = ARGMAX ? 16 : 1;
-  float rm[NB][1];
-  int bt[NB];
-  float bv[NB][kVals];
+  // Running state per lane and block: rm[b], the maximum so far; in the argmax variant also
+  // jx[b], the document token that holds it (the lowest row of the earliest tile on ties).  A
+  // tile whose maximum is strictly larger finds its row at once, so no tile values are kept.
+  float rm[NB];
+  int jx[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    rm[b][0] = -__builtin_huge_valf();
-    bt[b] = 0;
-#pragma unroll
-    for (int r = 0; r < kVals; ++r) bv[b][r] = 0.f;
+    rm[b] = -__builtin_huge_valf();
+    jx[b] = 0;
   }
   const int64_t n_entries = (int64_t)a.nq * a.lq;
   const int n_wg_q = (a.nq - qwg) < WPW * a.qpw ? (a.nq - qwg) : WPW * a.qpw;
@@ -312,39 +310,34 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_occupancy<KS, ARGMAX>())) void ma
 #pragma unroll
           for (int r = 2; r < 16; r += 2) m = fmaxf(fmaxf(m, acc[b][r]), acc[b][r + 1]);
           if (ARGMAX) {
-            const bool gt = m > rm[b][0];  // strict: the earlier tile keeps ties
-            rm[b][0] = gt ? m : rm[b][0];
-            bt[b] = gt ? t : bt[b];
+            if (m > rm[b]) {  // strict: the earlier tile keeps ties
+              int jr = 15;    // lowest row holding the maximum (rows ascend with r)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) bv[b][r] = gt ? acc[b][r] : bv[b][r];
+              for (int r = 14; r >= 0; --r) jr = acc[b][r] == m ? r : jr;
+              jx[b] = t * 32 + 8 * (jr >> 2) + row_base + (jr & 3);
+              rm[b] = m;
+            }
           } else {
-            rm[b][0] = fmaxf(rm[b][0], m);
+            rm[b] = fmaxf(rm[b], m);
           }
         }
-        if (last) {  // last tile of the document: reduce over rows and half-waves, emit
+        if (last) {  // last tile of the document: reduce over half-waves and slots, emit
           float qs = 0.f;
 #pragma unroll
           for (int b = 0; b < NB; ++b) {
-            float m;
-            if (ARGMAX) {
-              // lowest row of the best tile holding the maximum (rows ascend with r), then the
-              // lower token of the two half-waves
-              m = rm[b][0];
-              int jr = 15;
-#pragma unroll
-              for (int r = 14; r >= 0; --r) jr = bv[b][r] == m ? r : jr;
-              int jx = bt[b] * 32 + 8 * (jr >> 2) + row_base + (jr & 3);
+            float m = rm[b];
+            if (ARGMAX) {  // the lower token of the two half-waves on ties
+              int x = jx[b];
               const float om = __shfl_xor(m, 32);
-              const int oj = __shfl_xor(jx, 32);
-              const bool tk = beats(om, oj, m, jx);
+              const int ox = __shfl_xor(x, 32);
+              const bool tk = beats(om, ox, m, x);
               m = tk ? om : m;
-              jx = tk ? oj : jx;
-              if (half == 0 && slot_row[b] >= 0) res_amax[buf][j][slot_row[b]] = (uint16_t)jx;
-              rm[b][0] = -__builtin_huge_valf();
+              x = tk ? ox : x;
+              if (half == 0 && slot_row[b] >= 0) res_amax[buf][j][slot_row[b]] = (uint16_t)x;
             } else {
-              m = fmaxf(rm[b][0], __shfl_xor(rm[b][0], 32));
-              rm[b][0] = -__builtin_huge_valf();
+              m = fmaxf(m, __shfl_xor(m, 32));
             }
+            rm[b] = -__builtin_huge_valf();
             const float v = half32_sum(slot_row[b] >= 0 ? m : 0.f);
             if ((my_blocks >> b) & 1u) qs += v;
           }
@@ -482,7 +475,9 @@ bool maxsim_plan(int nq, int lq, int64_t n_docs, int64_t n_tok, int dim, bool ar
   // L2); the argmax variant, whose stores are short, takes one round of resident workgroups
   // (fewer per-workgroup prologues).  No range is shorter than ~1024 tokens (the query operands
   // are re-loaded by every workgroup).
-  const int occ = 2;  // resident workgroups per CU
+  // resident workgroups per CU: registers and LDS of the variant (the argmax variants at dim 33..64
+  // and above 128 stage more LDS per workgroup and fit two)
+  const int occ = argmax && (p->ks == 2 || p->ks == 8) ? 3 : 2;
   const int64_t target_wg = (int64_t)(n_cu > 0 ? n_cu : 256) * occ * (argmax ? 1 : 32);
   int64_t R = (target_wg + p->n_qgroups - 1) / p->n_qgroups;
   const int64_t max_by_tokens = n_tok / 1024 > 0 ? n_tok / 1024 : 1;
