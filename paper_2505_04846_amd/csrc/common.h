@@ -13,6 +13,15 @@ typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 
 constexpr int kWave = 64;
 
+// Address-space-qualified pointees for direct global-to-LDS loads (global_load_lds_dwordx4).
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
+
+// s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8):
+// wait until at most n vector-memory operations are outstanding, or until LDS/scalar ones are.
+constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+constexpr int kWaitLgkm0 = 15 | (3 << 14) | (7 << 4);
+
 __device__ __forceinline__ u32x4 load16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 
 __device__ __forceinline__ u32x4 load16_stream(const void* p) {

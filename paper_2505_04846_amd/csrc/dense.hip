@@ -32,8 +32,6 @@ namespace hpr {
 namespace {
 
 typedef __attribute__((ext_vector_type(16))) float f32x16;
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void glb_void_t;
 
 constexpr int kTQ = 256;       // queries per workgroup tile
 constexpr int kTR = 256;       // rows per workgroup tile
@@ -52,10 +50,6 @@ constexpr int kLoadsPerWave = kStageBytes / 1024 / kGemmWaves;  // 16-byte loads
 
 // 16 zero bytes in global memory: the source of the K-tail chunks past `dim`.
 __device__ __attribute__((aligned(16))) const uint32_t kZero16[4] = {0u, 0u, 0u, 0u};
-
-// s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
-constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
-constexpr int kWaitLgkm0 = 15 | (3 << 14) | (7 << 4);
 
 struct GemmArgs {
   const uint16_t* q;      // fp16 [nqa, dim]

@@ -112,7 +112,8 @@ __device__ __forceinline__ float half32_sum(float v) {
 // slots at three waves per SIMD: half the LDS operand reads per MFMA and half the query groups,
 // hence half the document-range re-reads).  Argmax: three (up to 168 VGPRs) with 64 slots per
 // wave, measured 10 % faster than two; 128 slots with the per-tile row search did not fit 256
-// VGPRs without spills and was slower.
+// VGPRs without spills and was slower, and so was a ring of three LDS stages filled by direct
+// global-to-LDS loads (no staging registers) at three workgroups per CU.
 template <int KS, bool ARGMAX>
 constexpr int maxsim_occupancy() { return ARGMAX ? 3 : 2; }
 
@@ -217,6 +218,7 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_occupancy<KS, ARGMAX>())) void ma
   const uint32_t lboff = 16u * lc;
   for (int i = tid; i < (int)(sizeof(lds) / 16); i += kThreads)
     reinterpret_cast<u32x4*>(&lds[0][0])[i] = u32x4{0u, 0u, 0u, 0u};
+  __syncthreads();  // the zeros land before any thread stores a tile over them
   const uint32_t row_bytes = 2u * (uint32_t)a.dim;
   auto fetch_stage = [&](StageDesc& sd) {
     sd.d0 = prod.d;
