@@ -33,20 +33,35 @@ namespace {
 
 typedef __attribute__((ext_vector_type(16))) float f32x16;
 
-constexpr int kTQ = 256;       // queries per workgroup tile
-constexpr int kTR = 256;       // rows per workgroup tile
-constexpr int kKC = 32;        // halves of K per stage
-constexpr int kStages = 4;     // LDS ring depth
-constexpr int kWQ = 4;         // waves along queries
-constexpr int kWR = 2;         // waves along rows
-constexpr int kBQ = kTQ / (32 * kWQ);  // 32-query blocks per wave
-constexpr int kBR = kTR / (32 * kWR);  // 32-row blocks per wave
-constexpr int kGemmWaves = kWQ * kWR;
-constexpr int kGemmThreads = 64 * kGemmWaves;
-constexpr int kRowBytes = kKC * 2;                      // 64
-constexpr int kTileBytes = kTQ * kRowBytes;             // 16 KiB per operand per stage
-constexpr int kStageBytes = 2 * kTileBytes;             // Q tile then X tile
-constexpr int kLoadsPerWave = kStageBytes / 1024 / kGemmWaves;  // 16-byte loads per lane
+// Workgroup tile geometry: TQ queries x 256 rows, WQ x WR waves, an NST-deep LDS ring of
+// K stages (32 halves each) holding the query tile then the row tile.
+template <int TQ, int WQ, int WR, int NST, int MIN_WG>
+struct GemmGeom {
+  static constexpr int kTQ = TQ;                    // queries per workgroup tile
+  static constexpr int kTR = 256;                   // rows per workgroup tile
+  static constexpr int kKC = 32;                    // halves of K per stage
+  static constexpr int kStages = NST;               // LDS ring depth
+  static constexpr int kWQ = WQ;                    // waves along queries
+  static constexpr int kWR = WR;                    // waves along rows
+  static constexpr int kBQ = kTQ / (32 * kWQ);      // 32-query blocks per wave
+  static constexpr int kBR = kTR / (32 * kWR);      // 32-row blocks per wave
+  static constexpr int kWaves = kWQ * kWR;
+  static constexpr int kThreads = 64 * kWaves;
+  static constexpr int kMinWG = MIN_WG;             // resident workgroups per CU to allow
+  static constexpr int kRowBytes = kKC * 2;         // 64
+  static constexpr int kQTileBytes = kTQ * kRowBytes;
+  static constexpr int kXTileBytes = kTR * kRowBytes;
+  static constexpr int kStageBytes = kQTileBytes + kXTileBytes;
+  static constexpr int kQLoads = kQTileBytes / 1024;              // 1 KiB wave-loads of queries
+  static constexpr int kLoadsPerWave = kStageBytes / 1024 / kWaves;  // 16-byte loads per lane
+  static_assert(kStageBytes % (1024 * kWaves) == 0, "a stage splits evenly over the waves");
+};
+// Many queries: 256 x 256 tiles, 8 waves of 64 x 128 (2 x 4 blocks), one workgroup per CU.
+using GeomWide = GemmGeom<256, 4, 2, 4, 1>;
+// At most 64 queries: 64 x 256 tiles, 4 waves of 64 x 64 (2 x 2 blocks), two workgroups per CU
+// (2 x 80 KiB of LDS).  The row stream is the bound there; the wide tile would multiply up to
+// 192 padding queries per row.
+using GeomNarrow = GemmGeom<64, 1, 4, 4, 2>;
 
 // 16 zero bytes in global memory: the source of the K-tail chunks past `dim`.
 __device__ __attribute__((aligned(16))) const uint32_t kZero16[4] = {0u, 0u, 0u, 0u};
@@ -71,8 +86,12 @@ struct GemmArgs {
   int64_t cap;
 };
 
-template <bool FILTER>
-__global__ __launch_bounds__(kGemmThreads, 1) void dense_gemm_kernel(GemmArgs a) {
+template <typename G, bool FILTER>
+__global__ __launch_bounds__(G::kThreads, G::kMinWG) void dense_gemm_kernel(GemmArgs a) {
+  constexpr int kTQ = G::kTQ, kTR = G::kTR, kKC = G::kKC, kStages = G::kStages;
+  constexpr int kWQ = G::kWQ, kBQ = G::kBQ, kBR = G::kBR;
+  constexpr int kRowBytes = G::kRowBytes, kQTileBytes = G::kQTileBytes;
+  constexpr int kStageBytes = G::kStageBytes, kLoadsPerWave = G::kLoadsPerWave;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -87,26 +106,26 @@ __global__ __launch_bounds__(kGemmThreads, 1) void dense_gemm_kernel(GemmArgs a)
   const int q_base = qt * kTQ;
   const int64_t row_base = a.r0 + (int64_t)rt * kTR;
 
-  // ---- this lane's direct-to-LDS sources: load j of the wave fills slot g = (4 w + j) 64 + l
-  // of the stage (slots 0..1023: the query tile, 1024..2047: the row tile).  The source is a
-  // wave-uniform base (the tile's first row, advanced by each stage's K offset) plus a 32-bit
-  // per-lane byte offset (row within the tile, clamped to the last valid row, and chunk).
-  const bool wave_x = wave * kLoadsPerWave * 64 >= 1024;  // uniform: waves 4..7 load the rows
-  const char* tile_base;
-  {
-    const int64_t first = wave_x ? row_base : (int64_t)q_base;
-    tile_base = reinterpret_cast<const char*>((wave_x ? a.x : a.q) + first * a.dim);
-  }
-  const int64_t tile_rows = wave_x ? (a.r1 - row_base) : (int64_t)(a.nqa - q_base);
+  // ---- this lane's direct-to-LDS sources: load j of the wave fills slot g = (L w + j) 64 + l
+  // of the stage (L loads per wave; the query tile's slots first, then the row tile's).  Whether
+  // a load reads queries or rows is uniform per (wave, j).  The source is a per-load base (the
+  // tile's first row, advanced by each stage's K offset) plus a 32-bit per-lane byte offset
+  // (row within the tile, clamped to the last valid row, and chunk).
+  const char* q_tile = reinterpret_cast<const char*>(a.q + (int64_t)q_base * a.dim);
+  const char* x_tile = reinterpret_cast<const char*>(a.x + row_base * a.dim);
+  const int64_t q_rows = (int64_t)(a.nqa - q_base), x_rows = a.r1 - row_base;
   uint32_t voff[kLoadsPerWave];
   int src_c[kLoadsPerWave];
+  bool is_x[kLoadsPerWave];
 #pragma unroll
   for (int j = 0; j < kLoadsPerWave; ++j) {
-    const int g = (wave * kLoadsPerWave + j) * 64 + lane;
-    const int local = g & 1023;
+    const int wl = wave * kLoadsPerWave + j;  // uniform
+    is_x[j] = wl >= G::kQLoads;
+    const int local = (is_x[j] ? wl - G::kQLoads : wl) * 64 + lane;
     int r = local >> 2;
     const int c = (local & 3) ^ ((r >> 2) & 3);
-    r = r < tile_rows ? r : (int)tile_rows - 1;
+    const int64_t rows = is_x[j] ? x_rows : q_rows;
+    r = r < rows ? r : (int)rows - 1;
     voff[j] = (uint32_t)r * (uint32_t)a.dim * 2u + 16u * c;
     src_c[j] = 8 * c;
   }
@@ -116,17 +135,18 @@ __global__ __launch_bounds__(kGemmThreads, 1) void dense_gemm_kernel(GemmArgs a)
   auto issue_stage = [&](int kk, int src_kk) {
     unsigned char* st = smem + (kk % kStages) * kStageBytes;
     const int k0 = src_kk * kKC;
-    const char* base = tile_base + 2 * (int64_t)k0;
+    const char* qb = q_tile + 2 * (int64_t)k0;
+    const char* xb = x_tile + 2 * (int64_t)k0;
     if (!k_tail || k0 + kKC <= a.dim) {
 #pragma unroll
       for (int j = 0; j < kLoadsPerWave; ++j)
-        __builtin_amdgcn_global_load_lds((glb_void_t*)(base + voff[j]),
+        __builtin_amdgcn_global_load_lds((glb_void_t*)((is_x[j] ? xb : qb) + voff[j]),
                                          (lds_void_t*)(st + (wave * kLoadsPerWave + j) * 1024),
                                          16, 0, 0);
     } else {  // the last, partial K chunk: chunks past `dim` read 16 zero bytes
 #pragma unroll
       for (int j = 0; j < kLoadsPerWave; ++j) {
-        const void* p = (k0 + src_c[j] < a.dim) ? (const void*)(base + voff[j])
+        const void* p = (k0 + src_c[j] < a.dim) ? (const void*)((is_x[j] ? xb : qb) + voff[j])
                                                  : (const void*)kZero16;
         __builtin_amdgcn_global_load_lds((glb_void_t*)p,
                                          (lds_void_t*)(st + (wave * kLoadsPerWave + j) * 1024),
@@ -149,7 +169,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void dense_gemm_kernel(GemmArgs a)
 #pragma unroll
     for (int b = 0; b < kBR; ++b) {
       const int r = wr * 32 * kBR + 32 * b + col;
-      offx[b][s] = kTileBytes + r * kRowBytes + 16 * (c ^ ((r >> 2) & 3));
+      offx[b][s] = kQTileBytes + r * kRowBytes + 16 * (c ^ ((r >> 2) & 3));
     }
   }
 
@@ -192,6 +212,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void dense_gemm_kernel(GemmArgs a)
   };
 
   Frags f0, f1;
+  static_assert(kStages == 4, "the waits below assume two stages in flight");
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * kLoadsPerWave));  // stage 0 landed (this wave)
   barrier();                                                // ... and for every wave
   read_frags(0, 0, f0);
@@ -402,10 +423,36 @@ __global__ void dense_zero_ctrl_kernel(int32_t* ctrl) { ctrl[0] = 0; }
 
 }  // namespace
 
+namespace {
+
+template <typename G>
+hipError_t launch_gemm_t(bool filter, GemmArgs a, int64_t n_rt, hipStream_t stream) {
+  a.n_qt = (a.nqa + G::kTQ - 1) / G::kTQ;
+  if (n_rt < 1 || n_rt > 0x7fffffffLL || (int64_t)a.n_qt * n_rt > 0xffffffffLL)
+    return hipErrorInvalidValue;
+  a.n_rt = (int)n_rt;
+  const int lds = G::kStages * G::kStageBytes;
+  const unsigned blocks = (unsigned)((int64_t)a.n_qt * n_rt);
+  const void* fn = filter ? (const void*)dense_gemm_kernel<G, true>
+                          : (const void*)dense_gemm_kernel<G, false>;
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) return e;
+  if (filter)
+    hipLaunchKernelGGL((dense_gemm_kernel<G, true>), dim3(blocks), dim3(G::kThreads), lds, stream,
+                       a);
+  else
+    hipLaunchKernelGGL((dense_gemm_kernel<G, false>), dim3(blocks), dim3(G::kThreads), lds,
+                       stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_dense_gemm(bool filter, const uint16_t* q, int nqa, const int32_t* qmap,
                              const uint16_t* x, int64_t r0, int64_t r1, int dim, float* scores,
                              int64_t ld, const float* theta, const int64_t* tie, int32_t* count,
                              float* cand_s, uint32_t* cand_i, int64_t cap, hipStream_t stream) {
+  if (nqa < 1) return hipErrorInvalidValue;
   GemmArgs a;
   a.q = q;
   a.x = x;
@@ -414,11 +461,6 @@ hipError_t launch_dense_gemm(bool filter, const uint16_t* q, int nqa, const int3
   a.dim = dim;
   a.r0 = r0;
   a.r1 = r1;
-  a.n_qt = (nqa + kTQ - 1) / kTQ;
-  const int64_t n_rt = (r1 - r0 + kTR - 1) / kTR;
-  if (nqa < 1 || n_rt < 1 || n_rt > 0x7fffffffLL || (int64_t)a.n_qt * n_rt > 0xffffffffLL)
-    return hipErrorInvalidValue;
-  a.n_rt = (int)n_rt;
   a.scores = scores;
   a.ld = ld;
   a.theta = theta;
@@ -427,16 +469,9 @@ hipError_t launch_dense_gemm(bool filter, const uint16_t* q, int nqa, const int3
   a.cand_s = cand_s;
   a.cand_i = cand_i;
   a.cap = cap;
-  const int lds = kStages * kStageBytes;
-  const unsigned blocks = (unsigned)((int64_t)a.n_qt * n_rt);
-  const void* fn = filter ? (const void*)dense_gemm_kernel<true> : (const void*)dense_gemm_kernel<false>;
-  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-  if (e != hipSuccess) return e;
-  if (filter)
-    hipLaunchKernelGGL(dense_gemm_kernel<true>, dim3(blocks), dim3(kGemmThreads), lds, stream, a);
-  else
-    hipLaunchKernelGGL(dense_gemm_kernel<false>, dim3(blocks), dim3(kGemmThreads), lds, stream, a);
-  return hipGetLastError();
+  const int64_t n_rt = (r1 - r0 + 255) / 256;
+  return nqa <= GeomNarrow::kTQ ? launch_gemm_t<GeomNarrow>(filter, a, n_rt, stream)
+                                : launch_gemm_t<GeomWide>(filter, a, n_rt, stream);
 }
 
 hipError_t launch_dense_init(const float* ss, int nq, int k, float* theta, int64_t* tie,

@@ -114,11 +114,25 @@ __device__ __forceinline__ float half32_sum(float v) {
 // wave, measured 10 % faster than two; 128 slots with the per-tile row search did not fit 256
 // VGPRs without spills and was slower, and so was a ring of three LDS stages filled by direct
 // global-to-LDS loads (no staging registers) at three workgroups per CU.
-template <int KS, bool ARGMAX>
-constexpr int maxsim_occupancy() { return ARGMAX ? 3 : 2; }
+//
+// Fewer query slots (small nq: NB = 1 or 2 blocks per wave) need fewer registers, and the
+// allocation allows three or four waves per SIMD: the kernel is then bound by the store stream,
+// which more resident workgroups keep in flight.
+constexpr int maxsim_waves(int ks, int nb, bool argmax) {
+  if (ks == 4 || ks == 16) return 2;  // their 64 KiB of stages fit two workgroups per CU anyway
+  return argmax ? 3 : (nb >= 4 ? 2 : nb == 2 ? 3 : 4);
+}
+// Workgroups per CU: the register bound above, and the LDS of two stages (plus under 4 KiB of
+// result buffers) against the CU's 160 KiB.
+constexpr int maxsim_resident(int ks, int nb, bool argmax) {
+  const int stage = (ks >= 8 ? 2 : 8) * 32 * ks * 32;
+  const int by_lds = (160 * 1024) / (2 * stage + 4096);
+  const int waves = maxsim_waves(ks, nb, argmax);
+  return waves < by_lds ? waves : by_lds;
+}
 
 template <int KS, int NB, int WPW, bool ARGMAX>
-__global__ __launch_bounds__(64 * WPW, (maxsim_occupancy<KS, ARGMAX>())) void maxsim_kernel(
+__global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB, ARGMAX))) void maxsim_kernel(
     MaxsimArgs a, const int64_t* __restrict__ off, const int64_t* __restrict__ part) {
   using G = TileGeom<KS>;
   constexpr int kThreads = 64 * WPW;
@@ -436,9 +450,9 @@ hipError_t launch_t(const MaxsimPlan& plan, const MaxsimArgs& args, hipStream_t 
   return hipGetLastError();
 }
 
-// Variants by k-steps of 16 (dim <= 16 KS).  Query slots per wave: 128 (plain, dim <= 128),
-// 64 (plain, dim 256; argmax, dim <= 128), 32 (argmax, dim 256) -- what fits two waves per
-// SIMD in 256 registers next to the argmax variants' 18 state registers per block.
+// Variants by k-steps of 16 (dim <= 16 KS) and query blocks per wave.  Query slots per wave:
+// plain 128 (dim <= 128) or 64 (dim 256), fewer when the call has few query slots; argmax 64
+// (dim <= 128) or 32 (dim 256).
 hipError_t launch_variant(const MaxsimPlan& plan, const MaxsimArgs& args, bool argmax,
                           hipStream_t stream) {
   if (argmax) {
@@ -450,11 +464,18 @@ hipError_t launch_variant(const MaxsimPlan& plan, const MaxsimArgs& args, bool a
       default: return hipErrorInvalidValue;
     }
   }
-  switch (plan.ks) {
-    case 2: return launch_t<2, 4, 4, false>(plan, args, stream);
-    case 4: return launch_t<4, 4, 4, false>(plan, args, stream);
-    case 8: return launch_t<8, 4, 4, false>(plan, args, stream);
-    case 16: return launch_t<16, 2, 4, false>(plan, args, stream);
+  switch (plan.ks * 8 + plan.nb) {
+    case 2 * 8 + 1: return launch_t<2, 1, 4, false>(plan, args, stream);
+    case 2 * 8 + 2: return launch_t<2, 2, 4, false>(plan, args, stream);
+    case 2 * 8 + 4: return launch_t<2, 4, 4, false>(plan, args, stream);
+    case 4 * 8 + 1: return launch_t<4, 1, 4, false>(plan, args, stream);
+    case 4 * 8 + 2: return launch_t<4, 2, 4, false>(plan, args, stream);
+    case 4 * 8 + 4: return launch_t<4, 4, 4, false>(plan, args, stream);
+    case 8 * 8 + 1: return launch_t<8, 1, 4, false>(plan, args, stream);
+    case 8 * 8 + 2: return launch_t<8, 2, 4, false>(plan, args, stream);
+    case 8 * 8 + 4: return launch_t<8, 4, 4, false>(plan, args, stream);
+    case 16 * 8 + 1: return launch_t<16, 1, 4, false>(plan, args, stream);
+    case 16 * 8 + 2: return launch_t<16, 2, 4, false>(plan, args, stream);
     default: return hipErrorInvalidValue;
   }
 }
@@ -466,20 +487,26 @@ bool maxsim_plan(int nq, int lq, int64_t n_docs, int64_t n_tok, int dim, bool ar
   if (dim < 8 || dim > 256 || dim % 8 != 0 || lq < 1 || nq < 1 || n_docs < 1) return false;
   p->ks = dim <= 32 ? 2 : dim <= 64 ? 4 : dim <= 128 ? 8 : 16;
   p->nb = argmax ? (p->ks == 16 ? 1 : 2) : (p->ks == 16 ? 2 : 4);
+  if (!argmax) {  // few query slots: fewer blocks per wave (never fewer than one query needs)
+    const int lqb = (lq + 31) / 32;
+    const int64_t slots = (int64_t)nq * lqb * 32;
+    int need = slots <= 32 * 4 ? 1 : slots <= 64 * 4 ? 2 : 4;
+    if (need < lqb) need = lqb;
+    need = need <= 1 ? 1 : need <= 2 ? 2 : 4;
+    if (need < p->nb) p->nb = need;
+  }
   p->wpw = 4;
   p->lqp = (lq + 31) / 32 * 32;
   if (p->lqp > p->nb * 32) return false;
   p->qpw = p->nb * 32 / p->lqp;
   const int64_t q_per_wg = (int64_t)p->qpw * p->wpw;
   p->n_qgroups = (int)((nq + q_per_wg - 1) / q_per_wg);
-  // Workgroups: the plain score takes enough to fill every CU's two resident slots 32 times
-  // over (short ranges keep the workgroups sharing a range in step, so the range is served from
-  // L2); the argmax variant, whose stores are short, takes one round of resident workgroups
-  // (fewer per-workgroup prologues).  No range is shorter than ~1024 tokens (the query operands
-  // are re-loaded by every workgroup).
-  // resident workgroups per CU: registers and LDS of the variant (the argmax variants at dim 33..64
-  // and above 128 stage more LDS per workgroup and fit two)
-  const int occ = argmax && (p->ks == 2 || p->ks == 8) ? 3 : 2;
+  // Workgroups: the plain score takes enough to fill every CU's resident slots 32 times over
+  // (short ranges keep the workgroups sharing a range in step, so the range is served from L2);
+  // the argmax variant, whose stores are short, takes one round of resident workgroups (fewer
+  // per-workgroup prologues).  No range is shorter than ~1024 tokens (the query operands are
+  // re-loaded by every workgroup).
+  const int occ = maxsim_resident(p->ks, p->nb, argmax);
   const int64_t target_wg = (int64_t)(n_cu > 0 ? n_cu : 256) * occ * (argmax ? 1 : 32);
   int64_t R = (target_wg + p->n_qgroups - 1) / p->n_qgroups;
   const int64_t max_by_tokens = n_tok / 1024 > 0 ? n_tok / 1024 : 1;

@@ -48,6 +48,8 @@ def _check_structure(s, i, n, k):
     (300, 2048, 4096, 100),
     (5, 1000, 8192, 1000),  # largest dim; k = n
     (3, 777, 24, 777),
+    (64, 3000, 128, 10),   # the widest narrow (64-query) tile
+    (65, 3000, 136, 10),   # the narrowest wide (256-query) tile
 ])
 def test_dense_topk_whole_store_sampled(nq, n, dim, k):
     Q, X = _rows(nq, dim, 1 + n), _rows(n, dim, 2 + n)
@@ -79,6 +81,18 @@ def test_dense_topk_filter_path_matches_oracle():
     for r, q in enumerate(pick):
         res = check_topk(s[q], i[q], O[r], k, rel=REL)
         assert res["exact"] or res["exception_used"]
+
+
+def test_dense_topk_filter_path_few_queries():
+    # at most 64 queries take the narrow tile in the sample and in the filtered scan
+    nq, n, dim, k = 17, 400_000, 256, 100
+    Q, X = _rows(nq, dim, 13), _rows(n, dim, 14)
+    s, i = hpr.dense_ip_topk(Q.to(DEV), X.to(DEV), k)
+    s, i = s.cpu().numpy(), i.cpu().numpy()
+    _check_structure(s, i, n, k)
+    O = oracle.dense_scores(_f16(Q), _f16(X))
+    for q in range(nq):
+        check_topk(s[q], i[q], O[q], k, rel=REL)
 
 
 def test_dense_topk_overflowing_lists_are_repaired():

@@ -97,6 +97,30 @@ def test_maxsim_scores_edge_shapes(nq, lq, lens, dim):
     _assert_close(S, O, rel=1e-4, what="scores (tight)")
 
 
+@pytest.mark.parametrize("nq,lq,dim,n_docs", [
+    (1, 32, 128, 5000),   # one block per wave: three idle waves per workgroup
+    (4, 32, 128, 3000),   # one block per wave, every wave active
+    (8, 32, 128, 3000),   # two blocks per wave
+    (2, 40, 128, 2000),   # a 64-slot query needs two blocks whatever the slot count
+    (1, 8, 64, 4000),
+    (3, 20, 256, 2000),
+    (6, 16, 32, 2500),
+])
+def test_maxsim_scores_few_queries(nq, lq, dim, n_docs):
+    # few query slots select the variants with fewer query blocks per wave and more resident
+    # workgroups; many documents give many short ranges
+    g = torch.Generator().manual_seed(nq * 1000 + lq)
+    lens = torch.randint(1, 300, (n_docs,), generator=g)
+    Q, D, off = _ragged(nq + lq + dim, nq, lq, lens.tolist(), dim)
+    S = hpr.maxsim_score(*_to_dev(Q, D, off)).cpu().numpy()
+    O = oracle.maxsim_scores(_bf(Q), _bf(D), off.numpy())
+    _assert_close(S, O, rel=1e-4, what="scores")
+    s, i = hpr.maxsim_topk(*_to_dev(Q, D, off), 50)
+    s, i = s.cpu().numpy(), i.cpu().numpy()
+    for q in range(nq):
+        check_topk(s[q], i[q], O[q], 50)
+
+
 def test_maxsim_many_ranges_and_query_groups():
     # enough documents and queries for several document ranges and query workgroups
     g = torch.Generator().manual_seed(7)
