@@ -18,8 +18,11 @@ Contents
   coltrast_total_loss          L = (L_LI + L_C) / 2 and its gradients (Sec. 3.2.1)
   dense_scores, dense_topk     inner-product / cosine retrieval on pooled embeddings (Sec. 3.2.1,
                                Sec. 4.2)
+  semantic_segments            semantic chunking boundaries by consecutive-sentence cosine
+                               (Sec. 3.2.2)
+  retrieval_metrics            P@k and MRR@k of a ranking with one positive per query (Sec. 4.2)
 
-Every function here is pinned by the CPU tests in tests/test_oracle_pins.py against hand-worked
+Every function here is pinned by the CPU tests (tests/test_oracle_*.py) against hand-worked
 fixtures, closed forms, invariants, brute force on tiny inputs and finite differences.
 """
 
@@ -28,6 +31,8 @@ from .maxsim import maxsim_scores, maxsim_argmax, rank_topk
 from .loss import coltrast_li_loss
 from .contrastive import contrastive_loss, coltrast_total_loss, pooled_means
 from .dense import dense_scores, dense_topk
+from .chunking import (chunk_cosines, semantic_segments, paper_starts, retrieval_ranks,
+                       retrieval_metrics)
 
 __all__ = [
     "decode_bf16",
@@ -41,4 +46,9 @@ __all__ = [
     "pooled_means",
     "dense_scores",
     "dense_topk",
+    "chunk_cosines",
+    "semantic_segments",
+    "paper_starts",
+    "retrieval_ranks",
+    "retrieval_metrics",
 ]
