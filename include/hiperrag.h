@@ -14,6 +14,10 @@
  *                          loss on the cosines of mean-pooled embeddings, with its gradients.
  *   dense_ip_topk          exact top-k rows of a pooled-embedding store by inner product
  *                          (= cosine for L2-normalised rows).
+ *   semantic_chunk         segment ids of a stream of sentence embeddings cut where the cosine
+ *                          of consecutive sentences is not above a threshold.
+ *   retrieval_metrics      P@k and MRR@k of retrieved index lists against one positive per
+ *                          query.
  *
  * Conventions shared by every entry point
  *   Pointers.  Every array argument is a DEVICE pointer on the current HIP device, owned by
@@ -73,6 +77,7 @@ typedef int32_t hpr_status;
  *     and every document has at most 65536 tokens (the latter is checked on the device: a
  *     longer document makes the loss NaN).
  *   dense_ip_topk: dim % 8 == 0, 8 <= dim <= 8192; n < 2^31.
+ *   semantic_chunk: dim % 8 == 0, 8 <= dim <= 4096; 1 <= n < 2^31.
  */
 
 /* ---------------------------------------------------------------------------------------------
@@ -195,6 +200,52 @@ hpr_status dense_ip_topk(const uint16_t* q, int32_t nq, const uint16_t* x, int64
                          int32_t dim, int32_t k, float* out_scores, int64_t* out_idx,
                          void* ws, size_t ws_bytes, void* stream);
 
+/* ---------------------------------------------------------------------------------------------
+ * semantic_chunk -- semantic chunking boundaries.
+ *
+ * The paper chunks each paper's text by walking its encoded sentences in order and growing a
+ * segment while the cosine similarity of consecutive sentences stays above a fixed threshold
+ * (Sec. 3.2.2, "ColTrast Finetuning Dataset").  Here, for sentence t of the input:
+ *     cos[t] = <E[t-1], E[t]> / (|E[t-1]| |E[t]|), NaN when t is the first sentence of its paper
+ *     boundary[t] = not (cos[t] > threshold)          (strict; NaN opens a segment)
+ *     seg[t] = (number of boundaries at or before t) - 1
+ * so the first sentence of every paper, and every sentence after (and of) a zero vector, opens a
+ * segment.  Arithmetic: fp16 x fp16 products accumulated in fp32 (v_dot2_f32_f16); the decision
+ * compares the fp32 cosine with the fp32 threshold.
+ *
+ *   emb        fp16 [n, dim] sentence embeddings, papers concatenated in order.
+ *   paper_off  int64 [n_papers + 1] paper offsets into the sentences (valid CSR: 0, ..., n;
+ *              empty papers allowed), or NULL for a single paper.  Not checked on the device;
+ *              invalid offsets give unspecified ids but no out-of-bounds access.
+ *   threshold  any non-NaN value.
+ *   cos_out    fp32 [n] output of the cosines, or NULL.
+ *   seg_out    int32 [n] output: segment ids, 0, 1, ... in sentence order.
+ *   n_segments int64 [1] output (device): the number of segments.
+ *   ws         workspace of semantic_chunk_workspace_size(n, dim) bytes.
+ * ------------------------------------------------------------------------------------------- */
+hpr_status semantic_chunk(const uint16_t* emb, int64_t n, int32_t dim, const int64_t* paper_off,
+                          int64_t n_papers, float threshold, float* cos_out, int32_t* seg_out,
+                          int64_t* n_segments, void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------------------------
+ * retrieval_metrics -- P@k and MRR@k of retrieval results with one positive per query.
+ *
+ * The paper evaluates retrieval by precision P = N_rel / N_ret with N_ret = k, and by
+ * MRR@k = (1/N_q) sum_q 1/rank_q, a term being zero when the positive is ranked beyond k
+ * (Sec. 4.2, "ColTrast Retrieval Evaluation").  With one positive per query, N_rel is 1 when the
+ * positive is among the first k retrieved indices; P@k is averaged over the queries.
+ *
+ *   topk_idx    int64 [nq, ld] retrieved indices per query, best first (e.g. maxsim_topk's or
+ *               dense_ip_topk's out_idx with ld = their k); the first k of each row are used.
+ *   positive    int64 [nq] the positive index of each query.
+ *   ranks_out   int32 [nq] output: 1-based rank of the positive, 0 when not within k; or NULL.
+ *   metrics_out fp64 [2] output (device): P@k, MRR@k (sums in fp64 in a fixed order).
+ * No workspace.
+ * ------------------------------------------------------------------------------------------- */
+hpr_status retrieval_metrics(const int64_t* topk_idx, int32_t nq, int32_t ld, int32_t k,
+                             const int64_t* positive, int32_t* ranks_out, double* metrics_out,
+                             void* stream);
+
 /* Workspace sizes in bytes for the calls above (0 is a valid size only when stated). */
 size_t maxsim_score_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int64_t n_tok,
                                    int32_t dim);
@@ -205,6 +256,7 @@ size_t coltrast_loss_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int6
 size_t coltrast_total_loss_workspace_size(int32_t nq, int32_t lq, int64_t n_docs, int64_t n_tok,
                                           int32_t dim);
 size_t dense_ip_topk_workspace_size(int32_t nq, int64_t n, int32_t dim, int32_t k);
+size_t semantic_chunk_workspace_size(int64_t n, int32_t dim);
 
 /* ---------------------------------------------------------------------------------------------
  * hpr_csr_validate -- checks a CSR offsets array on the device and SYNCHRONISES `stream`.
@@ -223,7 +275,7 @@ hpr_status hpr_scale_f32(float* x, int64_t n, const float* scale, void* stream);
  * bracketed by two HIP events recorded on its launch stream.  hpr_kernel_timing_read
  * synchronises on the events recorded for kernel `name` ("partition", "maxsim",
  * "maxsim_argmax", "topk", "infonce", "pool", "contrastive", "grad_q", "grad_d",
- * "dense_sample", "dense_scan", "dense_merge"), returns
+ * "dense_sample", "dense_scan", "dense_merge", "semantic_chunk", "retrieval_metrics"), returns
  * the sum of their durations in milliseconds and the launch count, and forgets them. */
 hpr_status hpr_kernel_timing(int32_t enable);
 hpr_status hpr_kernel_timing_read(const char* name, double* total_ms, int64_t* launches);

@@ -12,6 +12,8 @@ fallback: if the library is not built, or a call fails, an exception is raised.
                                                   -> dict(loss [3]: L, L_LI, L_C; dq, dd)
     coltrast_total_loss(Q, D, off, pos, scale, tau) -> L with autograd to Q and D
     dense_ip_topk(Q, X, k)                        -> (scores fp32 [nq, k], idx int64 [nq, k])
+    semantic_chunk(E, paper_off, threshold)       -> dict(seg int32 [n], n_segments, cos)
+    retrieval_metrics(idx, positive, k)           -> dict(p_at_k, mrr_at_k, ranks) on the device
     csr_validate(off, n_tok)                      -> (status name, first bad document or -1)
 
 Q and D are bf16 CUDA tensors ([nq, lq, dim] and [n_tok, dim]); off is int64 [n_docs + 1];
@@ -66,6 +68,9 @@ _SIGNATURES = {
     "coltrast_loss_workspace_size": (_SZ, [_I32, _I32, _I64, _I64, _I32]),
     "coltrast_total_loss_workspace_size": (_SZ, [_I32, _I32, _I64, _I64, _I32]),
     "dense_ip_topk_workspace_size": (_SZ, [_I32, _I64, _I32, _I32]),
+    "semantic_chunk": (_I32, [_P, _I64, _I32, _P, _I64, _F32, _P, _P, _P, _P, _SZ, _P]),
+    "semantic_chunk_workspace_size": (_SZ, [_I64, _I32]),
+    "retrieval_metrics": (_I32, [_P, _I32, _I32, _I32, _P, _P, _P, _P]),
     "hpr_csr_validate": (_I32, [_P, _I64, _I64, _P, _P, _P]),
     "hpr_scale_f32": (_I32, [_P, _I64, _P, _P]),
     "hpr_kernel_timing": (_I32, [_I32]),
@@ -314,6 +319,59 @@ def dense_ip_topk(Q, X, k, ws=None):
 def dense_workspace(Q, X, k):
     return _workspace(lib().dense_ip_topk_workspace_size(Q.shape[0], X.shape[0], Q.shape[1], k),
                       Q.device)
+
+
+def semantic_chunk(E, paper_off, threshold, return_cos=False, ws=None, out=None):
+    """Segment ids of fp16 sentence embeddings E [n, dim] (paper_off int64 [n_papers + 1] or
+    None for one paper).  Returns dict(seg int32 [n], n_segments int64 [1], cos fp32 [n] or None),
+    all on the device.  `out` may hold preallocated {"seg", "n_segments", "cos"}."""
+    _need(E, "E", torch.float16, 2)
+    dev = E.device
+    n, dim = E.shape
+    n_papers = 0
+    if paper_off is not None:
+        _need(paper_off, "paper_off", torch.int64, 1, dev)
+        n_papers = paper_off.numel() - 1
+    L = lib()
+    need = L.semantic_chunk_workspace_size(n, dim)
+    ws = ws if ws is not None and ws.numel() >= need else _workspace(need, dev)
+    out = {} if out is None else out
+    seg = out.get("seg")
+    if seg is None:
+        seg = torch.empty(n, dtype=torch.int32, device=dev)
+    n_seg = out.get("n_segments")
+    if n_seg is None:
+        n_seg = torch.empty(1, dtype=torch.int64, device=dev)
+    cos = out.get("cos") if return_cos else None
+    if return_cos and cos is None:
+        cos = torch.empty(n, dtype=torch.float32, device=dev)
+    with torch.cuda.device(dev):
+        _check(L.semantic_chunk(_ptr(E), n, dim, _ptr(paper_off), n_papers, float(threshold),
+                                _ptr(cos), _ptr(seg), _ptr(n_seg), _ptr(ws), ws.numel(),
+                                _stream(dev)))
+    return {"seg": seg, "n_segments": n_seg, "cos": cos}
+
+
+def semantic_chunk_workspace(E):
+    return _workspace(lib().semantic_chunk_workspace_size(E.shape[0], E.shape[1]), E.device)
+
+
+def retrieval_metrics(idx, positive, k=None):
+    """P@k and MRR@k of index lists idx int64 [nq, ld] against positive int64 [nq].  Returns
+    dict(metrics fp64 [2] = (P@k, MRR@k), ranks int32 [nq]) on the device."""
+    _need(idx, "idx", torch.int64, 2)
+    dev = idx.device
+    _need(positive, "positive", torch.int64, 1, dev)
+    nq, ld = idx.shape
+    k = ld if k is None else int(k)
+    if positive.numel() != nq:
+        raise ValueError("positive must hold one index per query")
+    metrics = torch.empty(2, dtype=torch.float64, device=dev)
+    ranks = torch.empty(nq, dtype=torch.int32, device=dev)
+    with torch.cuda.device(dev):
+        _check(lib().retrieval_metrics(_ptr(idx), nq, ld, k, _ptr(positive), _ptr(ranks),
+                                       _ptr(metrics), _stream(dev)))
+    return {"metrics": metrics, "ranks": ranks}
 
 
 def kernel_timing(enable):

@@ -20,7 +20,8 @@ BUILD_DIR = os.path.join(PKG_DIR, "_build")
 LIB_NAME = "libhiperrag.so"
 ARCH = "gfx950"
 
-SOURCES = ["abi.hip", "maxsim.hip", "topk.hip", "loss.hip", "contrastive.hip", "dense.hip"]
+SOURCES = ["abi.hip", "maxsim.hip", "topk.hip", "loss.hip", "contrastive.hip", "dense.hip",
+           "chunking.hip"]
 
 
 def _hipcc():

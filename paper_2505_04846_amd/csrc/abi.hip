@@ -348,6 +348,61 @@ hpr_status coltrast_total_loss_fwd_bwd(const uint16_t* q, int32_t nq, int32_t lq
                   loss, dq, dd, nullptr, ws, ws_bytes, stream);
 }
 
+size_t semantic_chunk_workspace_size(int64_t n, int32_t dim) {
+  (void)dim;
+  if (n < 1) return 0;
+  const int64_t R = chunk_ranges(n);
+  return align_up((size_t)R * sizeof(int32_t)) + align_up((size_t)R * sizeof(int64_t)) +
+         align_up((size_t)n * sizeof(float));
+}
+
+hpr_status semantic_chunk(const uint16_t* emb, int64_t n, int32_t dim, const int64_t* paper_off,
+                          int64_t n_papers, float threshold, float* cos_out, int32_t* seg_out,
+                          int64_t* n_segments, void* ws, size_t ws_bytes, void* stream) {
+  if (!emb || !seg_out || !n_segments || !ws)
+    return fail(HPR_ERR_INVALID_ARG, "emb, seg_out, n_segments and ws must be non-NULL");
+  if (n < 1 || n >= (int64_t(1) << 31))
+    return fail(HPR_ERR_INVALID_ARG, "n (%lld) must satisfy 1 <= n < 2^31", (long long)n);
+  if (dim % 8 != 0 || dim < 8 || dim > kMaxChunkDim)
+    return fail(HPR_ERR_UNSUPPORTED_SHAPE,
+                "semantic_chunk needs dim %% 8 == 0 and 8 <= dim <= %d (dim=%d)", kMaxChunkDim, dim);
+  if (!(threshold == threshold))
+    return fail(HPR_ERR_INVALID_ARG, "threshold must not be NaN");
+  if (paper_off && n_papers < 1)
+    return fail(HPR_ERR_INVALID_ARG, "n_papers (%lld) must be >= 1 with paper offsets",
+                (long long)n_papers);
+  if (!aligned16(emb)) return fail(HPR_ERR_INVALID_ARG, "emb must be 16-byte aligned");
+  const size_t need = semantic_chunk_workspace_size(n, dim);
+  if (ws_bytes < need)
+    return fail(HPR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu < %zu bytes", ws_bytes, need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Carver c(ws);
+  const int64_t R = chunk_ranges(n);
+  int32_t* cnt = c.take<int32_t>((size_t)R * sizeof(int32_t));
+  int64_t* base = c.take<int64_t>((size_t)R * sizeof(int64_t));
+  float* cos_ws = c.take<float>((size_t)n * sizeof(float));
+  hipError_t e = timed("semantic_chunk", s, [&] {
+    return launch_semantic_chunk(emb, n, dim, paper_off, paper_off ? n_papers : 0, threshold,
+                                 cos_out ? cos_out : cos_ws, cnt, base, seg_out, n_segments, s);
+  });
+  return e == hipSuccess ? HPR_OK : hip_fail(e, "semantic chunking launch");
+}
+
+hpr_status retrieval_metrics(const int64_t* topk_idx, int32_t nq, int32_t ld, int32_t k,
+                             const int64_t* positive, int32_t* ranks_out, double* metrics_out,
+                             void* stream) {
+  if (!topk_idx || !positive || !metrics_out)
+    return fail(HPR_ERR_INVALID_ARG, "topk_idx, positive and metrics_out must be non-NULL");
+  if (nq < 1) return fail(HPR_ERR_INVALID_ARG, "nq (%d) must be >= 1", nq);
+  if (k < 1 || k > ld)
+    return fail(HPR_ERR_INVALID_ARG, "k=%d must satisfy 1 <= k <= ld (%d)", k, ld);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = timed("retrieval_metrics", s, [&] {
+    return launch_retrieval_metrics(topk_idx, nq, ld, k, positive, ranks_out, metrics_out, s);
+  });
+  return e == hipSuccess ? HPR_OK : hip_fail(e, "retrieval metrics launch");
+}
+
 size_t dense_ip_topk_workspace_size(int32_t nq, int64_t n, int32_t dim, int32_t k) {
   if (nq < 1 || n < 1 || dim < 1 || k < 1) return 0;
   const DensePlan p = dense_plan(n, k);

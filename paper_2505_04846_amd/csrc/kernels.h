@@ -137,4 +137,21 @@ hipError_t launch_dense_merge(const float* ss, const int64_t* si, int nq_grid, i
 hipError_t launch_dense_repair_prep(const uint16_t* q, int dim, const int32_t* qlist, int m,
                                     uint16_t* qc, int32_t* count, hipStream_t stream);
 
+// Semantic chunking (chunking.hip): cos_out [n] (NaN at paper starts), seg [n] segment ids,
+// *n_seg the segment count; cnt [chunk_ranges(n)] int32 and base [chunk_ranges(n)] int64 are
+// scratch.  off (paper offsets, n_papers + 1 entries) may be null: one paper.  dim % 8 == 0,
+// 8 <= dim <= kMaxChunkDim.
+constexpr int kMaxChunkDim = 4096;
+constexpr int kRowsPerWave = 128;  // sentences per wave range
+int64_t chunk_ranges(int64_t n);
+hipError_t launch_semantic_chunk(const uint16_t* E, int64_t n, int dim, const int64_t* off,
+                                 int64_t n_papers, float thr, float* cos_out, int32_t* cnt,
+                                 int64_t* base, int32_t* seg, int64_t* n_seg,
+                                 hipStream_t stream);
+// P@k and MRR@k (out[0], out[1], fp64) and the 1-based rank of each positive (ranks, may be
+// null; 0 when absent) over the first k of the ld-strided index rows.
+hipError_t launch_retrieval_metrics(const int64_t* idx, int nq, int64_t ld, int k,
+                                    const int64_t* pos, int32_t* ranks, double* out,
+                                    hipStream_t stream);
+
 }  // namespace hpr

@@ -20,6 +20,8 @@ Workloads (sizes are the defaults; every generator takes smaller sizes for parit
                    cosine 0.95 to 1,000 distinct queries, top-100
   li_large         4,096 queries x 64 tokens vs 1,000,000 docs, Ld lognormal (median 200,
                    sigma 0.5) clipped to [16, 512], 10 % of docs noisy clones, top-1000
+  sentence_stream  10,000 papers of 50..350 sentence embeddings (dim 4096, fp16) whose topic
+                   changes after a geometric number of sentences (mean 8), for semantic chunking
 """
 
 import math
@@ -35,6 +37,7 @@ __all__ = [
     "li_retrieval",
     "dense_retrieval",
     "li_large",
+    "sentence_stream",
 ]
 
 _CHUNK_ROWS = 1 << 22
@@ -193,3 +196,46 @@ def li_large(seed=0, device="cpu", nq=4096, lq=64, n_docs=1_000_000, median=200.
             eps = torch.randn(base.shape, generator=gc, device=device, dtype=torch.float32)
             D[dst_rows[c0:c1]] = _normalise(base + clone_sigma * eps).to(torch.bfloat16)
     return {"Q": Q, "D": D, "off": off, "k": k, "clones": clones, "clone_src": src}
+
+
+def sentence_stream(seed=0, device="cpu", n_papers=10_000, len_min=50, len_max=350, dim=4096,
+                    topic_mean=8.0, sigma=0.5, chunk_rows=1 << 18):
+    """Sentence embeddings of consecutive papers (fp16 [n, dim], paper offsets int64).
+
+    Paper lengths are uniform in [len_min, len_max] (stream 3).  Within a paper the topic changes
+    after a geometric number of sentences with mean topic_mean (stream 5); every topic is a fresh
+    unit vector (stream 1), and a sentence is normalise(topic + sigma * g / sqrt(dim)) with g a
+    standard normal draw (stream 2), rounded to fp16.  Consecutive sentences of one topic then
+    have cosine ~ 1 / (1 + sigma^2) (0.8 at sigma = 0.5); of different topics ~ 0.
+    """
+    gl = stream_gen(seed, 3, device)
+    gt = stream_gen(seed, 5, device)
+    gu = stream_gen(seed, 1, device)
+    gn = stream_gen(seed, 2, device)
+    u = torch.rand(n_papers, generator=gl, device=device, dtype=torch.float64)
+    lens = (len_min + torch.floor(u * (len_max - len_min + 1))).to(torch.int64)
+    lens.clamp_(len_min, len_max)
+    off = csr_offsets(lens)
+    n = int(off[-1].item())
+    # topic switch before sentence t (t not a paper start) with probability 1 / topic_mean
+    switch = torch.rand(n, generator=gt, device=device) < (1.0 / topic_mean)
+    starts = off[:-1]
+    switch[starts[starts < n]] = True  # every non-empty paper opens with a new topic
+    topic = torch.cumsum(switch.to(torch.int64), 0) - 1
+    n_topics = int(topic[-1].item()) + 1
+    E = torch.empty((n, dim), dtype=torch.float16, device=device)
+    topics = torch.empty((0, dim), dtype=torch.float32, device=device)
+    t_lo = 0
+    for r0 in range(0, n, chunk_rows):
+        r1 = min(n, r0 + chunk_rows)
+        t_hi = int(topic[r1 - 1].item()) + 1
+        if t_hi > t_lo:  # the topics this chunk introduces, drawn in topic order
+            new = _normalise(torch.randn((t_hi - t_lo, dim), generator=gu, device=device,
+                                         dtype=torch.float32))
+            topics = torch.cat([topics[-1:], new]) if topics.numel() else new
+            base = t_lo - (1 if topics.shape[0] > t_hi - t_lo else 0)
+            t_lo = t_hi
+        tv = topics[topic[r0:r1] - base]
+        g = torch.randn((r1 - r0, dim), generator=gn, device=device, dtype=torch.float32)
+        E[r0:r1] = _normalise(tv + (sigma / math.sqrt(dim)) * g).to(torch.float16)
+    return {"E": E, "paper_off": off, "n_topics": n_topics, "threshold": 0.5}

@@ -127,6 +127,46 @@ def test_total_loss_workspace_holds_the_li_workspace():
     assert lib.coltrast_total_loss_workspace_size(0, 32, 512, 131072, 128) == 0
 
 
+def _chunk(**kw):
+    a = dict(emb=FAKE, n=1000, dim=4096, off=NULL, n_papers=0, thr=0.5, cos=NULL, seg=FAKE,
+             nseg=FAKE, ws=FAKE, ws_bytes=BIG)
+    a.update(kw)
+    return hpr.lib().semantic_chunk(a["emb"], a["n"], a["dim"], a["off"], a["n_papers"], a["thr"],
+                                    a["cos"], a["seg"], a["nseg"], a["ws"], a["ws_bytes"], NULL)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(emb=NULL), 1), (dict(seg=NULL), 1), (dict(nseg=NULL), 1), (dict(ws=NULL), 1),
+    (dict(n=0), 1), (dict(n=1 << 31), 1), (dict(dim=12), 4), (dict(dim=4104), 4), (dict(dim=0), 4),
+    (dict(thr=float("nan")), 1), (dict(off=FAKE, n_papers=0), 1), (dict(emb=FAKE_ODD), 1),
+    (dict(ws_bytes=16), 5),
+])
+def test_semantic_chunk_rejects(kw, status):
+    assert _chunk(**kw) == status
+    assert hpr.lib().hpr_last_error()
+
+
+def test_semantic_chunk_workspace():
+    lib = hpr.lib()
+    n = 2_000_000
+    w = lib.semantic_chunk_workspace_size(n, 4096)
+    ranges = (n + 127) // 128
+    assert w >= 4 * ranges + 8 * ranges + 4 * n and w % 256 == 0
+    assert lib.semantic_chunk_workspace_size(0, 4096) == 0
+    assert _chunk(n=n, ws_bytes=w - 1) == 5
+
+
+def test_retrieval_metrics_rejects():
+    lib = hpr.lib()
+    f = lib.retrieval_metrics
+    assert f(NULL, 4, 10, 10, FAKE, NULL, FAKE, NULL) == 1
+    assert f(FAKE, 4, 10, 10, NULL, NULL, FAKE, NULL) == 1
+    assert f(FAKE, 4, 10, 10, FAKE, NULL, NULL, NULL) == 1
+    assert f(FAKE, 0, 10, 10, FAKE, NULL, FAKE, NULL) == 1
+    assert f(FAKE, 4, 10, 11, FAKE, NULL, FAKE, NULL) == 1
+    assert f(FAKE, 4, 10, 0, FAKE, NULL, FAKE, NULL) == 1
+
+
 def test_workspace_sizes_are_consistent():
     lib = hpr.lib()
     s1 = lib.maxsim_score_workspace_size(64, 32, 512, 131072, 128)
