@@ -36,7 +36,8 @@ PEAK_HBM_GBS = 8000.0
 COPY_CALIBRATION_BYTES = 256 << 20  # bytes read (and written) by each calibration copy
 CPU_SAMPLE_SECONDS = 10.0  # the oracle sample is repeated for at least this long
 KERNELS = ("partition", "maxsim", "maxsim_argmax", "topk", "infonce", "pool", "contrastive",
-           "grad_q", "grad_d", "dense_sample", "dense_scan", "dense_merge")
+           "grad_q", "grad_d", "dense_sample", "dense_scan", "dense_merge", "semantic_chunk",
+           "retrieval_metrics")
 
 
 def parse():
@@ -46,7 +47,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="coltrast_step",
                     choices=["coltrast_step", "coltrast_total", "li_retrieval", "li_large",
-                             "dense_retrieval", "tiny_maxsim"])
+                             "dense_retrieval", "semantic_chunk", "tiny_maxsim"])
     ap.add_argument("--logit-scale", type=float, default=1.5625,
                     help="inverse temperature of the InfoNCE logits over MaxSim scores "
                          "(coltrast_step, coltrast_total)")
@@ -214,8 +215,10 @@ def build_workload(name, dev, scale, tau, nq_sub=None):
         n = X.shape[0]
         ws = hpr.dense_workspace(Q, X, k)
 
+        ws_out = {}
+
         def step():
-            hpr.dense_ip_topk(Q, X, k, ws=ws)
+            ws_out["scores"], ws_out["idx"] = hpr.dense_ip_topk(Q, X, k, ws=ws)
 
         sample_rows = min(n, max(131072, 32 * k))
         flops = 2.0 * dim * nq * float(n - sample_rows)  # the filtered scan over rows [S, n)
@@ -247,12 +250,62 @@ def build_workload(name, dev, scale, tau, nq_sub=None):
 
         cfg = {"workload": "dense_retrieval", "nq": nq, "n": n, "dim": dim, "k": k,
                "planted": int((w["planted_q"] < nq).sum()), "cosine": w["cosine"]}
+        sel = w["planted_q"] < nq
+        pq, pr = w["planted_q"][sel], w["planted_row"][sel]
+
+        def after():
+            # P@k and MRR@k of the planted pairs (each planted row is its query's positive) on
+            # the last step's output
+            if pq.numel() == 0:
+                return None
+            r = hpr.retrieval_metrics(ws_out["idx"][pq].contiguous(), pr.contiguous(), k)
+            m = r["metrics"].cpu().tolist()
+            return {"queries": int(pq.numel()), "k": k, "p_at_k": m[0], "mrr_at_k": m[1]}
         # the scan's algorithmic bytes: rows [S, n) and the queries read once
         sbytes = 2.0 * dim * float(n - sample_rows) + 2.0 * nq * dim
-        return dict(step=step, pairs=nq, kernel="dense_scan", flops=flops, bytes=sbytes,
+        return dict(step=step, pairs=nq, kernel="dense_scan", flops=flops, bytes=sbytes, after=after,
                     metric="top-k queries/sec + % fp16 MFMA peak",
                     cpu_sample=cpu_sample, config=cfg, dtype="fp16", unit="queries/s",
                     sha=source_sha("dense.hip", "common.h"), graph=False)
+
+    if name == "semantic_chunk":
+        w = synth.sentence_stream(seed=0, device=dev)
+        E, off, thr = w["E"], w["paper_off"], w["threshold"]
+        n, dim = E.shape
+        ws = hpr.semantic_chunk_workspace(E)
+        out = {"seg": torch.empty(n, dtype=torch.int32, device=dev),
+               "n_segments": torch.empty(1, dtype=torch.int64, device=dev)}
+
+        def step():
+            hpr.semantic_chunk(E, off, thr, ws=ws, out=out)
+
+        ranges = (n + 127) // 128
+        # every row read once (plus one halo row per 128-sentence range), the cosines written
+        # and read back, the segment ids written
+        cbytes = 2.0 * dim * (n + ranges) + 4.0 * n + 4.0 * n + 4.0 * n + 8.0 * (off.numel())
+        cflops = 4.0 * dim * n  # a squared norm and a dot product per sentence
+
+        def cpu_sample():
+            import numpy as np
+            import oracle
+            offh = off.cpu().numpy()
+            spent, p, done = 0.0, 0, 0
+            while p < offh.size - 1 and spent < CPU_SAMPLE_SECONDS:
+                a, b = int(offh[p]), int(offh[p + 1])
+                Eh = oracle.decode_fp16(E[a:b].cpu().view(torch.int16).numpy())
+                t0 = time.perf_counter()
+                oracle.semantic_segments(Eh, None, thr)
+                spent += time.perf_counter() - t0
+                done += b - a
+                p += 1
+            return done / spent, (f"the first {p} papers ({done} sentences), one at a time")
+
+        cfg = {"workload": "semantic_chunk", "n_sentences": n, "n_papers": int(off.numel() - 1),
+               "dim": dim, "threshold": thr, "topic_mean": 8.0, "sigma": 0.5}
+        return dict(step=step, pairs=n, kernel="semantic_chunk", flops=cflops, bytes=cbytes,
+                    metric="semantic chunking sentences/sec + % HBM BW", cpu_sample=cpu_sample,
+                    config=cfg, dtype="fp16", unit="sentences/s",
+                    sha=source_sha("chunking.hip", "common.h"))
 
     raise SystemExit(f"workload {name} is not available in this build")
 
@@ -320,6 +373,13 @@ def main():
         torch.cuda.synchronize()
         graph_ms = start.elapsed_time(stop) / args.steps
 
+    extra = None
+    if W.get("after"):
+        W["after"]()  # first call: code-object load and warm caches, untimed
+        torch.cuda.synchronize()
+        hpr.kernel_timing(True)
+        extra = W["after"]()
+        hpr.kernel_timing(False)
     kernels = {}
     for name in KERNELS:
         tot, n = hpr.kernel_timing_read(name)
@@ -392,6 +452,7 @@ def main():
         "roofline": roofline,
         "roofline_topk": roofline_topk,
         "cpu_baseline": cpu,
+        "retrieval_metrics": extra,
         "kernels": kernels,
         "eager": {"ms_per_step": ms, "value": W["pairs"] / (ms * 1e-3)},
         "graph_replay": None if graph_ms is None else {

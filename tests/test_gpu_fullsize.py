@@ -164,3 +164,36 @@ def test_dense_retrieval_fullsize():
               f"{t_c:.6f}, exact order {res['exact']}, tolerance exception {res['exception_used']}")
     del w, Q, X
     torch.cuda.empty_cache()
+
+
+def test_semantic_chunk_fullsize():
+    # the benchmark's stream (10,000 papers, ~2M sentences of dim 4096) through the benchmark's
+    # call: every id is the prefix count of the GPU's own decisions, and sampled cosines (paper
+    # starts, their neighbours and random sentences) are checked against the oracle one by one
+    w = synth.sentence_stream(seed=0, device=DEV)
+    E, off, thr = w["E"], w["paper_off"], w["threshold"]
+    n = E.shape[0]
+    r = hpr.semantic_chunk(E, off, thr, return_cos=True)
+    cos = r["cos"]
+    bnd = ~(cos > thr)
+    seg_want = torch.cumsum(bnd.to(torch.int64), 0) - 1
+    assert torch.equal(r["seg"].to(torch.int64), seg_want)
+    assert int(r["n_segments"].item()) == int(bnd.sum().item())
+    g = torch.Generator().manual_seed(0)
+    starts = off[:-1][off[:-1] < n]
+    pick = torch.cat([starts[:200], (starts[1:201] - 1), starts[:200] + 1,
+                      torch.randint(0, n, (1500,), generator=g, device="cpu").to(DEV)])
+    pick = torch.unique(pick.clamp(0, n - 1)).cpu().numpy()
+    offh = off.cpu().numpy()
+    first = np.zeros(n, dtype=bool)
+    first[offh[:-1][offh[:-1] < n]] = True
+    cg = cos.cpu().numpy().astype(np.float64)
+    for t in pick:
+        if first[t]:
+            assert np.isnan(cg[t]), t
+            continue
+        Eh = oracle.decode_fp16(E[t - 1:t + 1].cpu().view(torch.int16).numpy())
+        o = oracle.chunk_cosines(Eh)[1]
+        assert abs(cg[t] - o) <= 2e-5, (t, cg[t], o)
+        if abs(o - thr) > 2e-5:
+            assert bool(cg[t] > thr) == bool(o > thr), t
