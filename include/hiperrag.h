@@ -271,11 +271,24 @@ hpr_status hpr_csr_validate(const int64_t* d_off, int64_t n_docs, int64_t n_tok,
  * upstream gradient to the gradients of the loss calls without a host round trip. */
 hpr_status hpr_scale_f32(float* x, int64_t n, const float* scale, void* stream);
 
+/* Calibration for benchmarks: what the device sustains, to report beside the published peaks.
+ *   hpr_mfma_calibration  launches a kernel of 8 waves per CU, each running `iters` iterations
+ *                         of four independent v_mfma_f32_32x32x16_bf16 on register operands (no
+ *                         memory traffic); *flops [host] receives its FLOP count.  sink: device
+ *                         fp32 [4096] scratch.  Time it on `stream` (or with
+ *                         hpr_kernel_timing_read("mfma_calibration")).
+ *   hpr_read_calibration  streams `bytes` (a positive multiple of 16) of device memory at `buf`
+ *                         with 16-byte loads.  sink: device uint32 [16384] scratch.  Timing
+ *                         name "read_calibration". */
+hpr_status hpr_mfma_calibration(int64_t iters, float* sink, double* flops, void* stream);
+hpr_status hpr_read_calibration(const void* buf, int64_t bytes, uint32_t* sink, void* stream);
+
 /* Per-kernel timing for benchmarks.  While enabled, every kernel the library launches is
  * bracketed by two HIP events recorded on its launch stream.  hpr_kernel_timing_read
  * synchronises on the events recorded for kernel `name` ("partition", "maxsim",
  * "maxsim_argmax", "topk", "infonce", "pool", "contrastive", "grad_q", "grad_d",
- * "dense_sample", "dense_scan", "dense_merge", "semantic_chunk", "retrieval_metrics"), returns
+ * "dense_sample", "dense_scan", "dense_merge", "semantic_chunk", "retrieval_metrics",
+ * "mfma_calibration", "read_calibration"), returns
  * the sum of their durations in milliseconds and the launch count, and forgets them. */
 hpr_status hpr_kernel_timing(int32_t enable);
 hpr_status hpr_kernel_timing_read(const char* name, double* total_ms, int64_t* launches);

@@ -21,7 +21,7 @@ LIB_NAME = "libhiperrag.so"
 ARCH = "gfx950"
 
 SOURCES = ["abi.hip", "maxsim.hip", "topk.hip", "loss.hip", "contrastive.hip", "dense.hip",
-           "chunking.hip"]
+           "chunking.hip", "calibration.hip"]
 
 
 def _hipcc():

@@ -403,6 +403,34 @@ hpr_status retrieval_metrics(const int64_t* topk_idx, int32_t nq, int32_t ld, in
   return e == hipSuccess ? HPR_OK : hip_fail(e, "retrieval metrics launch");
 }
 
+hpr_status hpr_mfma_calibration(int64_t iters, float* sink, double* flops, void* stream) {
+  if (!sink || !flops) return fail(HPR_ERR_INVALID_ARG, "sink and flops must be non-NULL");
+  if (iters < 1 || iters > (int64_t(1) << 32))
+    return fail(HPR_ERR_INVALID_ARG, "iters (%lld) must be in [1, 2^32]", (long long)iters);
+  int n_cu = 0;
+  hpr_status st = current_cu_count(&n_cu);
+  if (st != HPR_OK) return st;
+  *flops = (double)mfma_calibration_waves(n_cu) * (double)iters * 4.0 * 32768.0;
+  hipError_t e = timed("mfma_calibration", static_cast<hipStream_t>(stream), [&] {
+    return launch_mfma_calibration(sink, iters, n_cu, static_cast<hipStream_t>(stream));
+  });
+  return e == hipSuccess ? HPR_OK : hip_fail(e, "MFMA calibration launch");
+}
+
+hpr_status hpr_read_calibration(const void* buf, int64_t bytes, uint32_t* sink, void* stream) {
+  if (!buf || !sink) return fail(HPR_ERR_INVALID_ARG, "buf and sink must be non-NULL");
+  if (bytes < 16 || bytes % 16 != 0 || !aligned16(buf))
+    return fail(HPR_ERR_INVALID_ARG, "bytes must be a positive multiple of 16, buf 16-byte aligned");
+  int n_cu = 0;
+  hpr_status st = current_cu_count(&n_cu);
+  if (st != HPR_OK) return st;
+  const int blocks = n_cu * 32 < 16384 ? n_cu * 32 : 16384;  // 8 waves per SIMD
+  hipError_t e = timed("read_calibration", static_cast<hipStream_t>(stream), [&] {
+    return launch_read_calibration(buf, bytes, sink, blocks, static_cast<hipStream_t>(stream));
+  });
+  return e == hipSuccess ? HPR_OK : hip_fail(e, "read calibration launch");
+}
+
 size_t dense_ip_topk_workspace_size(int32_t nq, int64_t n, int32_t dim, int32_t k) {
   if (nq < 1 || n < 1 || dim < 1 || k < 1) return 0;
   const DensePlan p = dense_plan(n, k);

@@ -154,4 +154,13 @@ hipError_t launch_retrieval_metrics(const int64_t* idx, int nq, int64_t ld, int 
                                     const int64_t* pos, int32_t* ranks, double* out,
                                     hipStream_t stream);
 
+// Calibration (calibration.hip): a pure-MFMA kernel of mfma_calibration_waves(n_cu) waves, each
+// running `iters` iterations of four v_mfma_f32_32x32x16_bf16 (sink: at least one float per
+// 4-wave workgroup); a pure streaming read of `bytes` (a multiple of 16) with `blocks`
+// workgroups (sink: one word per workgroup).
+int64_t mfma_calibration_waves(int n_cu);
+hipError_t launch_mfma_calibration(float* sink, int64_t iters, int n_cu, hipStream_t stream);
+hipError_t launch_read_calibration(const void* buf, int64_t bytes, uint32_t* sink, int blocks,
+                                   hipStream_t stream);
+
 }  // namespace hpr

@@ -167,6 +167,18 @@ def test_retrieval_metrics_rejects():
     assert f(FAKE, 4, 10, 0, FAKE, NULL, FAKE, NULL) == 1
 
 
+def test_calibration_rejects_bad_arguments():
+    lib = hpr.lib()
+    flops = ctypes.c_double(0)
+    assert lib.hpr_mfma_calibration(0, FAKE, ctypes.byref(flops), NULL) == 1
+    assert lib.hpr_mfma_calibration(10, NULL, ctypes.byref(flops), NULL) == 1
+    assert lib.hpr_mfma_calibration(10, FAKE, None, NULL) == 1
+    assert lib.hpr_read_calibration(NULL, 1024, FAKE, NULL) == 1
+    assert lib.hpr_read_calibration(FAKE, 1000, FAKE, NULL) == 1
+    assert lib.hpr_read_calibration(FAKE_ODD, 1024, FAKE, NULL) == 1
+    assert lib.hpr_read_calibration(FAKE, 1024, NULL, NULL) == 1
+
+
 def test_workspace_sizes_are_consistent():
     lib = hpr.lib()
     s1 = lib.maxsim_score_workspace_size(64, 32, 512, 131072, 128)
