@@ -3,7 +3,8 @@
 //   mfma_calibration_kernel  every wave runs four independent accumulation chains of
 //                            v_mfma_f32_32x32x16_bf16 on register operands (no memory traffic)
 //                            for a fixed number of iterations: 4 * 32768 FLOP per iteration.
-//   read_calibration_kernel  a grid-stride stream of 16-byte loads over a buffer, folded with
+//   read_calibration_kernel  a grid-stride stream of 16-byte streaming (non-temporal) loads
+//                            over a buffer, folded with
 //                            integer adds (so the loads cannot be dropped), one word per
 //                            workgroup written: the sustained HBM read rate.
 // Both end after a fixed amount of work; nothing they compute is meaningful beyond keeping the
@@ -50,7 +51,7 @@ __global__ __launch_bounds__(kCalThreads) void read_calibration_kernel(const u32
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
       const int64_t i = base + u * stride;
-      v[u] = i < n16 ? p[i] : u32x4{0u, 0u, 0u, 0u};
+      v[u] = i < n16 ? __builtin_nontemporal_load(p + i) : u32x4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
     for (int u = 0; u < kU; ++u) acc += v[u].x + v[u].y + v[u].z + v[u].w;
