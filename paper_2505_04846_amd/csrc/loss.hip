@@ -272,51 +272,57 @@ __global__ void grad_q_reduce_kernel(const float* __restrict__ part, int R, int6
   grad_q_sum_ranges(part, R, i0, i1, n4, dq, dqc, lq, dim);
 }
 
-constexpr int kGdWaves = 16;
-constexpr int kGdThreads = 64 * kGdWaves;
-constexpr int kGdCols = 32;        // dD columns a thread owns (4 chunks of 8)
-constexpr int kGdBatch = 4;        // entries whose Q rows a thread loads at once
+constexpr int kGdThreads = 256;
+constexpr int kGdWaves = kGdThreads / 64;
+constexpr int kGdRows = 512;        // rows of a document sorted per pass
+constexpr int kGdBatch = 8;         // positions whose Q rows a group has in flight (x2)
 constexpr int kGdMaxStageQ = 4096;  // G[:, d] is staged in LDS when nq is at most this
 
-// TPR threads own one dD row (chunk c of the row, 8 columns, belongs to thread c % TPR), so a
-// pass covers RPP = 1024 / TPR rows of a document.
-__host__ __device__ inline int gd_tpr(int dim) { return dim <= 64 ? 2 : dim <= 128 ? 4 : 8; }
+// TPE threads read one Q row, CPT chunks of 16 bytes (8 columns) each: chunk c + TPE i of the
+// row belongs to thread c of its group (dim <= 8 TPE CPT); kGdThreads / TPE groups.  Fewer,
+// wider threads per entry spread the per-position bookkeeping over more columns.
+__host__ __device__ inline int gd_cpt(int dim) { return dim <= 64 ? 1 : dim <= 128 ? 2 : 4; }
+__host__ __device__ inline int gd_tpe(int dim) { return 8; }
 
 // LDS layout of grad_d_kernel (bytes, each part 16-byte aligned).
 struct GdLds {
-  int keys, sorted, cnt, rs, gcol, total;
+  int keys, sorted, weight, cnt, rs, gcol, total;
 };
-__host__ __device__ inline GdLds gd_lds(int E, int nq, int rpp) {
+__host__ __device__ inline GdLds gd_lds(int E, int nq) {
   GdLds l;
   l.keys = 0;  // the document's argmax entries, staged once
   l.sorted = (2 * E + 15) / 16 * 16;
-  l.cnt = l.sorted + (2 * E + 15) / 16 * 16;
-  l.rs = l.cnt + kGdWaves * rpp * 4;
-  l.gcol = l.rs + ((rpp + 1) * 4 + 15) / 16 * 16;
+  l.weight = l.sorted + 4 * E;
+  l.cnt = l.weight + 4 * E;
+  l.rs = l.cnt + kGdWaves * kGdRows * 4;
+  l.gcol = l.rs + ((kGdRows + 1) * 4 + 15) / 16 * 16;
   l.total = l.gcol + (nq <= kGdMaxStageQ ? (4 * nq + 15) / 16 * 16 : 0);
   return l;
 }
 
 // dD: one workgroup per document d.  Entry e = q * lq + i selected token a(e) = amax[d][e] of
 // the document; dD[j] = sum over the entries with a(e) = j, in entry order, of G[q,d] Q[e].
-// The argmax entries (and G[:, d]) are staged in LDS.  Per pass over RPP rows:
+// The argmax entries (and G[:, d]) are staged in LDS.  Per pass over kGdRows rows:
 //   1. a stable counting sort of the entries by token -- per-wave histograms over contiguous
-//      entry ranges, a prefix scan, a ballot-ranked scatter in entry order -- gives each row
-//      its entries, in entry order;
-//   2. the TPR threads of row j keep its columns in registers and walk its entries, kGdBatch at
-//      a time, gathering their Q rows straight from L2 (the TPR threads of a row read 16 * TPR
-//      contiguous bytes per load);
-//   3. each row is written once -- zeros for rows nobody selected.
+//      entry ranges, a prefix scan, a ballot-ranked scatter in entry order -- lists each row's
+//      entries contiguously, in entry order, with their weights G[q,d];
+//   2. the sorted list is cut into one contiguous slice per group of TPE threads, at row
+//      boundaries, each slice holding about the same number of entries (a row never
+//      straddles two slices);
+//   3. each group walks its slice in order, gathering whole 256-byte Q rows (TPE x 16 bytes,
+//      straight from L2) kGdBatch positions ahead of the ones it adds, and writes each row once
+//      it is complete -- zeros (or the contrastive part) for rows nobody selected.
 // Deterministic: every row sums its entries in entry order, with no atomics on floats.
-template <int TPR>
-__global__ __launch_bounds__(kGdThreads) void grad_d_kernel(
+template <int TPE, int CPT>
+__global__ __launch_bounds__(kGdThreads, 2) void grad_d_kernel(
     const uint16_t* __restrict__ Q, const int64_t* __restrict__ off, int64_t n_docs,
     int64_t n_tok, int dim, int nq, int lq, uint64_t lq_magic,
     const uint16_t* __restrict__ amax, const float* __restrict__ G, float* __restrict__ dd,
     const float* __restrict__ dq_part, int dq_R, float* __restrict__ dq,
     const float* __restrict__ dqc, const float* __restrict__ ddc) {
   extern __shared__ __attribute__((aligned(16))) unsigned char gd_smem[];
-  constexpr int RPP = kGdThreads / TPR;
+  constexpr int kGroups = kGdThreads / TPE;
+  constexpr int kRpt = kGdRows / kGdThreads;  // rows per thread in the scan
   if (dq_part) {  // the dQ range sums, one slice per workgroup (independent of the rest)
     const int64_t n4 = (int64_t)nq * lq * dim / 4;
     const int64_t per = (n4 + gridDim.x - 1) / gridDim.x;
@@ -324,13 +330,15 @@ __global__ __launch_bounds__(kGdThreads) void grad_d_kernel(
     grad_q_sum_ranges(dq_part, dq_R, i0, i0 + per < n4 ? i0 + per : n4, n4, dq, dqc, lq, dim);
   }
   const int E = nq * lq;
-  const GdLds L = gd_lds(E, nq, RPP);  // the same layout the launcher sized for this TPR
+  const GdLds L = gd_lds(E, nq);  // the same layout the launcher sized
   uint16_t* am = reinterpret_cast<uint16_t*>(gd_smem + L.keys);
-  uint16_t* sorted = reinterpret_cast<uint16_t*>(gd_smem + L.sorted);
+  uint32_t* spk = reinterpret_cast<uint32_t*>(gd_smem + L.sorted);
+  float* sw = reinterpret_cast<float*>(gd_smem + L.weight);
   int* cnt = reinterpret_cast<int*>(gd_smem + L.cnt);
   int* rs = reinterpret_cast<int*>(gd_smem + L.rs);
   float* gcol = reinterpret_cast<float*>(gd_smem + L.gcol);
   __shared__ int wave_tot[kGdWaves];
+  __shared__ int bounds[kGroups + 1];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t d = blockIdx.x;
@@ -355,27 +363,53 @@ __global__ __launch_bounds__(kGdThreads) void grad_d_kernel(
   const int eb = wave * epw < E ? wave * epw : E;
   const int ee = eb + epw < E ? eb + epw : E;
   const uint64_t lt_mask = (1ull << lane) - 1ull;
-  const int j = tid / TPR;          // row of this thread within the pass
-  const int cp = tid - j * TPR;     // its chunk phase: chunks cp, cp + TPR, ...
+  const int grp = tid / TPE;
+  const int c = tid - grp * TPE;  // this thread's chunks: columns 8 (c + TPE i) .. + 7
+  bool cok[CPT];
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) cok[i] = 8 * (c + TPE * i) < dim;
+  // the document's contrastive part (the same for each of its rows), or zeros
+  float init[8 * CPT];
+#pragma unroll
+  for (int v = 0; v < 8 * CPT; ++v) init[v] = 0.f;
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    if (ddc && cok[i]) {
+      const float* src = ddc + d * dim + 8 * (c + TPE * i);
+      const f32x4 v0 = *reinterpret_cast<const f32x4*>(src);
+      const f32x4 v1 = *reinterpret_cast<const f32x4*>(src + 4);
+      init[8 * i + 0] = v0.x; init[8 * i + 1] = v0.y; init[8 * i + 2] = v0.z;
+      init[8 * i + 3] = v0.w; init[8 * i + 4] = v1.x; init[8 * i + 5] = v1.y;
+      init[8 * i + 6] = v1.z; init[8 * i + 7] = v1.w;
+    }
+  }
 
-  for (int64_t w0 = 0; w0 < len; w0 += RPP) {
-    const int Wn = (int)(len - w0 < RPP ? len - w0 : RPP);
+  for (int64_t w0 = 0; w0 < len; w0 += kGdRows) {
+    const int Wn = (int)(len - w0 < kGdRows ? len - w0 : kGdRows);
     int nbits = 0;
     while ((1 << nbits) < Wn) ++nbits;
-    for (int k = lane; k < Wn; k += 64) cnt[wave * RPP + k] = 0;
+    for (int k = lane; k < Wn; k += 64) cnt[wave * kGdRows + k] = 0;
     __syncthreads();
     // per-wave histogram of the pass's tokens
     for (int e = eb + lane; e < ee; e += 64) {
       const int key = (int)am[e] - (int)w0;
-      if (key >= 0 && key < Wn) atomicAdd(&cnt[wave * RPP + key], 1);
+      if (key >= 0 && key < Wn) atomicAdd(&cnt[wave * kGdRows + key], 1);
     }
     __syncthreads();
-    // exclusive scan over (token, wave) in token-major order; thread t owns token t
+    // exclusive scan over (token, wave) in token-major order; thread t owns kRpt tokens
     {
-      int tot = 0;
-      if (tid < Wn)
-        for (int w = 0; w < kGdWaves; ++w) tot += cnt[w * RPP + tid];
-      int incl = tot;
+      const int r_begin = tid * kRpt;
+      int tot[kRpt];
+      int sum = 0;
+#pragma unroll
+      for (int i = 0; i < kRpt; ++i) {
+        const int row = r_begin + i;
+        tot[i] = 0;
+        if (row < Wn)
+          for (int w = 0; w < kGdWaves; ++w) tot[i] += cnt[w * kGdRows + row];
+        sum += tot[i];
+      }
+      int incl = sum;
 #pragma unroll
       for (int o = 1; o < 64; o <<= 1) {
         const int y = __shfl_up(incl, o);
@@ -385,20 +419,26 @@ __global__ __launch_bounds__(kGdThreads) void grad_d_kernel(
       __syncthreads();
       int before = 0;
       for (int w = 0; w < wave; ++w) before += wave_tot[w];
-      const int excl = before + incl - tot;
-      if (tid < Wn) {
-        int run = excl;
-        for (int w = 0; w < kGdWaves; ++w) {
-          const int c = cnt[w * RPP + tid];
-          cnt[w * RPP + tid] = run;
-          run += c;
+      int run = before + incl - sum;
+#pragma unroll
+      for (int i = 0; i < kRpt; ++i) {
+        const int row = r_begin + i;
+        if (row < Wn) {
+          rs[row] = run;
+          int r2 = run;
+          for (int w = 0; w < kGdWaves; ++w) {
+            const int cw = cnt[w * kGdRows + row];
+            cnt[w * kGdRows + row] = r2;
+            r2 += cw;
+          }
+          run += tot[i];
         }
-        rs[tid] = excl;
-        if (tid == Wn - 1) rs[Wn] = excl + tot;
       }
+      if (tid == kGdThreads - 1) rs[Wn] = before + incl;
     }
     __syncthreads();
-    // stable scatter: in entry order within the wave, ranked among equal tokens by ballots
+    // stable scatter: in entry order within the wave, ranked among equal tokens by ballots;
+    // each position also receives its entry's weight
     for (int base = eb; base < ee; base += 64) {
       const int e = base + lane;
       int key = -1;
@@ -413,79 +453,124 @@ __global__ __launch_bounds__(kGdThreads) void grad_d_kernel(
       if (valid) {
         const int rank = __popcll(peers & lt_mask);
         const int n = __popcll(peers);
-        const int start = cnt[wave * RPP + key];
-        sorted[start + rank] = (uint16_t)e;
-        if (rank == 0) cnt[wave * RPP + key] = start + n;
+        const int start = cnt[wave * kGdRows + key];
+        const uint32_t qq = (uint32_t)(((uint64_t)e * lq_magic) >> 32);
+        spk[start + rank] = (uint32_t)e | ((uint32_t)key << 16);
+        sw[start + rank] = g_staged ? gcol[qq] : G[(int64_t)qq * n_docs + d];
+        if (rank == 0) cnt[wave * kGdRows + key] = start + n;
       }
     }
     __syncthreads();
-
-    // row j's entries, kGdBatch at a time (absent entries repeat a valid one with weight 0),
-    // added to the document's contrastive part (the same for each of its rows) when there is one
-    float acc[kGdCols];
-#pragma unroll
-    for (int v = 0; v < kGdCols; ++v) acc[v] = 0.f;
-    if (ddc) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int c = cp + TPR * i;
-        if (8 * c < dim) {
-          const f32x4 v0 = *reinterpret_cast<const f32x4*>(ddc + d * dim + 8 * c);
-          const f32x4 v1 = *reinterpret_cast<const f32x4*>(ddc + d * dim + 8 * c + 4);
-          acc[8 * i + 0] = v0.x;
-          acc[8 * i + 1] = v0.y;
-          acc[8 * i + 2] = v0.z;
-          acc[8 * i + 3] = v0.w;
-          acc[8 * i + 4] = v1.x;
-          acc[8 * i + 5] = v1.y;
-          acc[8 * i + 6] = v1.z;
-          acc[8 * i + 7] = v1.w;
+    // slices: group g takes rows [bounds[g], bounds[g + 1]), cut where the sorted positions
+    // pass g / kGroups of the pass's entries
+    if (tid <= kGroups) {
+      const int n = rs[Wn];
+      int r = tid == 0 ? 0 : Wn;
+      if (tid > 0 && tid < kGroups) {
+        const int target = (int)(((int64_t)tid * n + kGroups - 1) / kGroups);
+        int a = 0, b = Wn;  // first row whose entries start at or after the target
+        while (a < b) {
+          const int mid = (a + b) >> 1;
+          if (rs[mid] < target)
+            a = mid + 1;
+          else
+            b = mid;
         }
+        r = a;
+      }
+      bounds[tid] = r;
+    }
+    __syncthreads();
+
+    // ---- the group's walk over its slice of positions [p0, p1), in order.  Every position
+    // carries its entry and row; a row is written when the next position belongs to another
+    // row.  Positions past the slice are padding (weight 0, row kNoRow) and write nothing.
+    {
+      constexpr uint32_t kNoRow = 0xffffu;
+      const int p0 = rs[bounds[grp]];
+      const int p1 = rs[bounds[grp + 1]];
+      float* drow0 = dd + (lo + w0) * dim + 8 * c;
+      auto write_row = [&](uint32_t row, const float (&v)[8 * CPT]) {
+#pragma unroll
+        for (int i = 0; i < CPT; ++i) {
+          if (cok[i]) {
+            float* dst = drow0 + (int64_t)row * dim + 8 * TPE * i;
+            *reinterpret_cast<f32x4*>(dst) =
+                f32x4{v[8 * i], v[8 * i + 1], v[8 * i + 2], v[8 * i + 3]};
+            *reinterpret_cast<f32x4*>(dst + 4) =
+                f32x4{v[8 * i + 4], v[8 * i + 5], v[8 * i + 6], v[8 * i + 7]};
+          }
+        }
+      };
+      float acc[8 * CPT];
+#pragma unroll
+      for (int v = 0; v < 8 * CPT; ++v) acc[v] = init[v];
+      // two batches of positions in flight: the next one is loaded while this one is added
+      constexpr int kB = CPT >= 4 ? 4 : 8;  // positions per batch
+      u32x4 wb[2][kB][CPT];
+      float gb[2][kB];
+      uint32_t rb[2][kB];
+      auto load_batch = [&](int slot, int pb) {
+#pragma unroll
+        for (int u = 0; u < kB; ++u) {
+          const int pos = pb + u;
+          const bool ok = pos < p1;
+          const uint32_t pk = spk[ok ? pos : p0];
+          rb[slot][u] = ok ? pk >> 16 : kNoRow;
+          gb[slot][u] = ok ? sw[pos] : 0.f;
+          const uint16_t* qrow = Q + (int64_t)(pk & 0xffffu) * dim;
+#pragma unroll
+          for (int i = 0; i < CPT; ++i) {  // columns past dim re-read the row's last chunk
+            const int col = 8 * (c + TPE * i) < dim ? 8 * (c + TPE * i) : dim - 8;
+            wb[slot][u][i] = load16(qrow + col);
+          }
+        }
+      };
+      auto add_batch = [&](int slot, uint32_t next_row) {
+#pragma unroll
+        for (int u = 0; u < kB; ++u) {
+          const float g = gb[slot][u];
+#pragma unroll
+          for (int i = 0; i < CPT; ++i) {
+            const u32x4 w = wb[slot][u][i];
+            acc[8 * i + 0] += g * bf16_lo(w.x);
+            acc[8 * i + 1] += g * bf16_hi(w.x);
+            acc[8 * i + 2] += g * bf16_lo(w.y);
+            acc[8 * i + 3] += g * bf16_hi(w.y);
+            acc[8 * i + 4] += g * bf16_lo(w.z);
+            acc[8 * i + 5] += g * bf16_hi(w.z);
+            acc[8 * i + 6] += g * bf16_lo(w.w);
+            acc[8 * i + 7] += g * bf16_hi(w.w);
+          }
+          const uint32_t row = rb[slot][u];
+          const uint32_t nrow = u + 1 < kB ? rb[slot][u + 1] : next_row;
+          if (row != nrow && row != kNoRow) {  // the row's last entry: write it
+            write_row(row, acc);
+#pragma unroll
+            for (int v = 0; v < 8 * CPT; ++v) acc[v] = init[v];
+          }
+        }
+      };
+      if (p0 < p1) load_batch(0, p0);
+      for (int pb = p0; pb < p1; pb += 2 * kB) {
+        const bool more1 = pb + kB < p1;
+        if (more1) load_batch(1, pb + kB);
+        add_batch(0, more1 ? rb[1][0] : kNoRow);
+        if (!more1) break;
+        const bool more0 = pb + 2 * kB < p1;
+        if (more0) load_batch(0, pb + 2 * kB);
+        add_batch(1, more0 ? rb[0][0] : kNoRow);
       }
     }
-    if (j < Wn) {
-      const int p_end = rs[j + 1];
-      for (int p = rs[j]; p < p_end; p += kGdBatch) {
-        u32x4 w[kGdBatch][4];
-        float g[kGdBatch];
-#pragma unroll
-        for (int b = 0; b < kGdBatch; ++b) {
-          const bool ok = p + b < p_end;
-          const uint32_t e = sorted[ok ? p + b : p];
-          const uint32_t qq = (uint32_t)(((uint64_t)e * lq_magic) >> 32);
-          const float gv = g_staged ? gcol[qq] : G[(int64_t)qq * n_docs + d];
-          g[b] = ok ? gv : 0.f;
-          const uint16_t* qrow = Q + (int64_t)e * dim;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int c = cp + TPR * i;  // chunk: columns 8c .. 8c + 7
-            w[b][i] = 8 * c < dim ? load16(qrow + 8 * c) : u32x4{0u, 0u, 0u, 0u};
-          }
-        }
-#pragma unroll
-        for (int b = 0; b < kGdBatch; ++b)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            acc[8 * i + 0] += g[b] * bf16_lo(w[b][i].x);
-            acc[8 * i + 1] += g[b] * bf16_hi(w[b][i].x);
-            acc[8 * i + 2] += g[b] * bf16_lo(w[b][i].y);
-            acc[8 * i + 3] += g[b] * bf16_hi(w[b][i].y);
-            acc[8 * i + 4] += g[b] * bf16_lo(w[b][i].z);
-            acc[8 * i + 5] += g[b] * bf16_hi(w[b][i].z);
-            acc[8 * i + 6] += g[b] * bf16_lo(w[b][i].w);
-            acc[8 * i + 7] += g[b] * bf16_hi(w[b][i].w);
-          }
-      }
-      float* drow = dd + (lo + w0 + j) * dim;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int c = cp + TPR * i;
-        if (8 * c < dim) {
-          *reinterpret_cast<f32x4*>(drow + 8 * c) =
-              f32x4{acc[8 * i], acc[8 * i + 1], acc[8 * i + 2], acc[8 * i + 3]};
-          *reinterpret_cast<f32x4*>(drow + 8 * c + 4) =
-              f32x4{acc[8 * i + 4], acc[8 * i + 5], acc[8 * i + 6], acc[8 * i + 7]};
-        }
+    // rows nobody selected: their value is the document's contrastive part (or zero), one
+    // thread per row
+    for (int r = tid; r < Wn; r += kGdThreads) {
+      if (rs[r] != rs[r + 1]) continue;
+      float* dst = dd + (lo + w0 + r) * dim;
+      for (int k = 0; k < dim; k += 4) {
+        f32x4 v = {0.f, 0.f, 0.f, 0.f};
+        if (ddc) v = *reinterpret_cast<const f32x4*>(ddc + d * dim + k);
+        *reinterpret_cast<f32x4*>(dst + k) = v;
       }
     }
     __syncthreads();  // the pass's LDS is reused by the next one
@@ -543,18 +628,18 @@ hipError_t launch_grad_q(const uint16_t* d_tok, const int64_t* off, int64_t n_do
   return hipGetLastError();
 }
 
-template <int TPR>
+template <int TPE, int CPT>
 hipError_t launch_grad_d_t(const uint16_t* q, const int64_t* off, int64_t n_docs, int64_t n_tok,
                            int dim, int nq, int lq, uint64_t magic, const uint16_t* amax,
                            const float* G, float* dd, const float* dq_part, int dq_R, float* dq,
                            const float* dqc, const float* ddc, hipStream_t stream) {
-  const int lds = gd_lds(nq * lq, nq, kGdThreads / TPR).total;
+  const int lds = gd_lds(nq * lq, nq).total;
   if (lds > 65536) {  // beyond the default dynamic LDS limit (large nq * lq only)
-    const hipError_t e = hipFuncSetAttribute((const void*)grad_d_kernel<TPR>,
+    const hipError_t e = hipFuncSetAttribute((const void*)grad_d_kernel<TPE, CPT>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(grad_d_kernel<TPR>, dim3((unsigned)n_docs), dim3(kGdThreads), lds, stream, q,
+  hipLaunchKernelGGL((grad_d_kernel<TPE, CPT>), dim3((unsigned)n_docs), dim3(kGdThreads), lds, stream, q,
                      off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, dqc,
                      ddc);
   return hipGetLastError();
@@ -569,10 +654,10 @@ hipError_t launch_grad_d(const uint16_t* q, const int64_t* off, int64_t n_docs, 
   // floor(e / lq) = (e * ceil(2^32 / lq)) >> 32 for e < 2^14 and lq <= 128: the product
   // overshoots e / lq by less than e / 2^32 < 2^-18, below the 1 / lq gap to the next integer.
   const uint64_t magic = (0x100000000ull + (uint64_t)lq - 1) / (uint64_t)lq;
-  switch (gd_tpr(dim)) {
-    case 2: return launch_grad_d_t<2>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, dqc, ddc, stream);
-    case 4: return launch_grad_d_t<4>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, dqc, ddc, stream);
-    case 8: return launch_grad_d_t<8>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, dqc, ddc, stream);
+  switch (gd_tpe(dim) * 8 + gd_cpt(dim)) {
+    case 8 * 8 + 1: return launch_grad_d_t<8, 1>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, dqc, ddc, stream);
+    case 8 * 8 + 2: return launch_grad_d_t<8, 2>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, dqc, ddc, stream);
+    case 8 * 8 + 4: return launch_grad_d_t<8, 4>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, dqc, ddc, stream);
     default: return hipErrorInvalidValue;
   }
 }
