@@ -15,7 +15,7 @@
 //     8 (i / 4) + 4 (l / 32) + i % 4, i = 0..15 (document tokens).  The plain score folds each
 //     tile's 16 values into one running max per lane with v_max3 (8 instructions per tile and
 //     block); the argmax variant also folds them into one integer key that carries the lowest
-//     row holding the maximum (tile_key), and keeps the tile of the best key (the document
+//     row holding the maximum (the tile keys below), and keeps the tile of the best key (the document
 //     token is kept, not the tile's values), which leaves room for three resident workgroups
 //     per CU.  At the end of a document the two half-waves are combined and the slot maxima
 //     summed per query.
@@ -83,34 +83,18 @@ struct StageDesc {
   uint32_t valid, last, lng;
 };
 
-// Argmax key of one 32x32 tile column: the lane's 16 values v_r (r = 0..15, rows ascending
-// with r) as order-preserving integers o(v) (o(v) = bits of v for v >= 0, bits ^ 0x7fffffff
-// below zero: increasing in v) with the low 4 bits replaced by 15 - r.  The signed maximum of the
-// keys is then the largest o(v) & ~15 held by the lowest row, in one bitop3 per value plus one
-// three-way max per two values (a compare-and-select search of the 16 rows costs about twice
-// as many instructions).  The row selected is the first one whose value equals the maximum up
-// to its 4 lowest mantissa bits (a relative window below 2^-19); the score itself takes the
-// exact maximum.  For v >= 0, o(v) = bits(v): a lane whose tile holds a non-negative value needs
+// Argmax keys ("tile keys") of one 32x32 tile column: the lane's 16 values v_r (r = 0..15,
+// rows ascending with r) as order-preserving integers o(v) (o(v) = bits of v for v >= 0,
+// bits ^ 0x7fffffff below zero: increasing in v) with the low 4 bits replaced by 15 - r.  The
+// signed maximum of the keys is then the largest o(v) & ~15 held by the lowest row, in one
+// v_bitop3 per value ((bits & ~15) | (15 - r), truth table 0xea: a & b | c) plus one three-way
+// max per two values (a compare-and-select search of the 16 rows costs about twice as many
+// instructions).  The row selected is the first one whose value equals the maximum up to its 4
+// lowest mantissa bits (a relative window below 2^-19); the score itself takes the exact
+// maximum.  For v >= 0, o(v) = bits(v): a lane whose tile holds a non-negative value needs
 // nothing else; a lane whose 16 values are all negative (its key is then negative) redoes the
-// keys with the sign-flipped encoding.
+// keys with the sign-flipped encoding, key ^ 0x7ffffff0.
 __device__ __forceinline__ int max3_i(int a, int b, int c) { return max(max(a, b), c); }
-__device__ __forceinline__ int tile_key(const f32x16& acc) {
-  int k[16];
-#pragma unroll
-  for (int r = 0; r < 16; ++r)  // (bits & ~15) | (15 - r) as one v_bitop3 (table 0xea: a & b | c)
-    k[r] = __builtin_amdgcn_bitop3_b32(__float_as_int(acc[r]), ~15, 15 - r, 0xea);
-  int m = max(k[0], k[1]);
-#pragma unroll
-  for (int r = 2; r < 16; r += 2) m = max3_i(m, k[r], k[r + 1]);
-  if (m < 0) {  // every value of this lane's tile is negative
-#pragma unroll
-    for (int r = 0; r < 16; ++r) k[r] ^= 0x7ffffff0;  // = ((bits ^ 0x7fffffff) & ~15) | (15 - r)
-    m = max(k[0], k[1]);
-#pragma unroll
-    for (int r = 2; r < 16; r += 2) m = max3_i(m, k[r], k[r + 1]);
-  }
-  return m;
-}
 
 // Cross-lane moves within a row of 16 lanes through DPP (no LDS round trip).
 template <int CTRL>
@@ -396,7 +380,7 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB))) void maxsim_kerne
 
 // ---------------------------------------------------------------------------------------------
 // MaxSim with the argmax (the loss forward), software-pipelined.  The epilogue of a tile (the
-// running maximum, the packed argmax keys of tile_key and their maximum) costs about half as
+// running maximum, the packed argmax tile keys and their maximum) costs about half as
 // many issue cycles as the tile's MFMAs, so each wave keeps two accumulator sets: the MFMAs of
 // tile t are issued interleaved with the epilogue of tile t - 1 (sched_group_barrier pattern:
 // one A operand read per k-step, then per MFMA a few VALU instructions), and one wave keeps the
@@ -594,7 +578,8 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
   // The tile is processed in kRegions scheduling regions of kRs k-steps each (at most 4, so
   // that only two sets of A fragments are live); region p of the epilogue covers registers
   // [kRv p, kRv (p + 1)) of every block of Y: the tile maximum mt, the packed argmax keys k (see
-  // tile_key) and their maximum mk; the last region also updates the running maximum.
+  // the tile keys above) and their maximum mk; the last region also updates the running
+  // maximum.
   constexpr int kRs = KS / 2 < 4 ? KS / 2 : 4;
   constexpr int kRegions = KS / kRs;
   constexpr int kRv = 16 / kRegions;
@@ -618,19 +603,25 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
     }
   };
   // Rest of the epilogue: lanes whose tile is all negative (one branch for every block, taken
-  // by rare waves: the keys and maxima it reads stay in the interleaved region), the key
-  // update, the end of a document.
-  auto epi_finish = [&](const float (&mt)[NB], const int (&k)[NB][16], int (&mk)[NB],
+  // by rare waves; it recomputes the keys from Y, whose registers are live until the next
+  // step, so that the region's 16 keys per block need not stay live past it), the key update,
+  // the end of a document.
+  auto epi_finish = [&](const f32x16 (&Y)[NB], const float (&mt)[NB], int (&mk)[NB],
                         const PendTile& p) {
     bool neg = false;
 #pragma unroll
     for (int b = 0; b < NB; ++b) neg |= mt[b] < 0.f;
-    if (neg) {
+    if (__ballot(neg) != 0) {  // a wave-uniform branch: no exec-mask save and restore
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
-        int x = max(k[b][0] ^ 0x7ffffff0, k[b][1] ^ 0x7ffffff0);  // sign-flipped keys
+        int kn[16];  // sign-flipped keys: ((bits ^ 0x7fffffff) & ~15) | (15 - r)
 #pragma unroll
-        for (int r = 2; r < 16; r += 2) x = max3_i(x, k[b][r] ^ 0x7ffffff0, k[b][r + 1] ^ 0x7ffffff0);
+        for (int r = 0; r < 16; ++r)
+          kn[r] = __builtin_amdgcn_bitop3_b32(__float_as_int(Y[b][r]), ~15, 15 - r, 0xea) ^
+                  0x7ffffff0;
+        int x = max(kn[0], kn[1]);
+#pragma unroll
+        for (int r = 2; r < 16; r += 2) x = max3_i(x, kn[r], kn[r + 1]);
         mk[b] = mt[b] < 0.f ? x : mk[b];
       }
     }
@@ -746,7 +737,7 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
         int k[NB][16], mk[NB];
         if (pend) {
           step(std::true_type{}, X, Y, buf, j, fr, mt, k, mk);
-          epi_finish(mt, k, mk, pt);
+          epi_finish(Y, mt, mk, pt);
         } else {
           step(std::false_type{}, X, Y, buf, j, fr, mt, k, mk);
         }
@@ -770,14 +761,15 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
   if (wave_active && pend) {
     float mt[NB];
     int k[NB][16], mk[NB];
+    if (pend_in_a) {
 #pragma unroll
-    for (int p = 0; p < kRegions; ++p) {
-      if (pend_in_a)
-        epi_part(accA, p, mt, k, mk);
-      else
-        epi_part(accB, p, mt, k, mk);
+      for (int p = 0; p < kRegions; ++p) epi_part(accA, p, mt, k, mk);
+      epi_finish(accA, mt, mk, pt);
+    } else {
+#pragma unroll
+      for (int p = 0; p < kRegions; ++p) epi_part(accB, p, mt, k, mk);
+      epi_finish(accB, mt, mk, pt);
     }
-    epi_finish(mt, k, mk, pt);
   }
   __syncthreads();
   if (stage >= 1) write_results(prv, (stage - 1) % 3);
