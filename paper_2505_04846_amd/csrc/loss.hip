@@ -169,8 +169,11 @@ __global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
 
   // Documents in chunks of 32.  First, lane l loads the row index and weight of two of the
   // wave's four entries (2 (l >> 5) and the next) against document l & 31 of the chunk -- one
-  // round trip for the chunk's metadata; then each 16-lane group gathers its entry's rows,
-  // 16 documents at a time, taking the metadata from the lanes that loaded it.
+  // round trip for the chunk's metadata -- into the wave's table in LDS; then each 16-lane
+  // group gathers its entry's rows, 16 documents at a time, reading each document's (row,
+  // weight) with one LDS load that the group's lanes share.  Only the wave itself reads its
+  // table, and a wave's LDS accesses complete in order.
+  __shared__ int2 meta[kGqWaves][4][32];
   const int mu = lane & 31, mh = lane >> 5;
   const int k = lane >> 4;  // this lane's entry within the wave
   for (int64_t db = d0; db < d1; db += 32) {
@@ -187,7 +190,9 @@ __global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
       const int64_t rr = base + (ok ? amax[dm * E + ek] : 0);
       rowm[t] = (int)(rr > last_tok ? last_tok : rr);
       gm[t] = ok ? G[(ek / lq) * n_docs + dm] : 0.f;
+      meta[wave][2 * mh + t][mu] = make_int2(rowm[t], __float_as_int(gm[t]));
     }
+    __builtin_amdgcn_wave_barrier();
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
       if (db + 16 * half >= d1) break;  // uniform
@@ -195,11 +200,9 @@ __global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
       float g[16];
 #pragma unroll
       for (int uu = 0; uu < 16; ++uu) {
-        const int src = 16 * half + uu + 32 * (k >> 1);
-        const int rA = __shfl(rowm[0], src), rB = __shfl(rowm[1], src);
-        const float gA = __shfl(gm[0], src), gB = __shfl(gm[1], src);
-        const int64_t row = (k & 1) ? rB : rA;
-        g[uu] = (k & 1) ? gB : gA;
+        const int2 mt = meta[wave][k][16 * half + uu];
+        const int64_t row = mt.x;
+        g[uu] = __int_as_float(mt.y);
 #pragma unroll
         for (int cc = 0; cc < CPL; ++cc) {
           const int kk = 8 * (c + 16 * cc);
@@ -220,6 +223,7 @@ __global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
           acc[cc][7] += g[uu] * bf16_hi(w[uu][cc].w);
         }
     }
+    __builtin_amdgcn_wave_barrier();  // the table is rewritten by the next chunk
   }
   if (!active) return;
   float* dst = (direct ? dq : part + (int64_t)r * E * dim) + e * dim;  // direct: final sums
