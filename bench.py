@@ -146,7 +146,8 @@ def build_workload(name, dev, scale, tau, nq_sub=None):
                        pooling="mean over tokens")
         return dict(step=step, pairs=nq * n_docs, kernel="maxsim_argmax", flops=flops,
                     cpu_sample=cpu_sample, config=cfg, dtype="bf16", unit="pairs/s",
-                    sha=source_sha("maxsim.hip", "common.h"), graph_primary=True)
+                    sha=source_sha("maxsim_argmax.hip", "maxsim_common.h", "common.h"),
+                    graph_primary=True)
 
     if name in ("li_retrieval", "li_large", "tiny_maxsim"):
         if name == "li_retrieval":
@@ -203,7 +204,7 @@ def build_workload(name, dev, scale, tau, nq_sub=None):
         mbytes = 2.0 * dim * n_tok + 2.0 * nq * lq * dim + 8.0 * (n_docs + 1) + 4.0 * nq * n_docs
         return dict(step=step, pairs=nq * n_docs, kernel="maxsim", flops=flops, bytes=mbytes,
                     cpu_sample=cpu_sample, config=cfg, dtype="bf16", unit="pairs/s",
-                    sha=source_sha("maxsim.hip", "common.h"),
+                    sha=source_sha("maxsim.hip", "maxsim_common.h", "common.h"),
                     topk_bytes=4.0 * nq * n_docs + 12.0 * nq * k)
 
     if name == "dense_retrieval":

@@ -20,8 +20,8 @@ BUILD_DIR = os.path.join(PKG_DIR, "_build")
 LIB_NAME = "libhiperrag.so"
 ARCH = "gfx950"
 
-SOURCES = ["abi.hip", "maxsim.hip", "topk.hip", "loss.hip", "contrastive.hip", "dense.hip",
-           "chunking.hip", "calibration.hip"]
+SOURCES = ["abi.hip", "maxsim.hip", "maxsim_argmax.hip", "topk.hip", "loss.hip", "contrastive.hip",
+           "dense.hip", "chunking.hip", "calibration.hip"]
 
 
 def _hipcc():
@@ -48,7 +48,7 @@ COMMON_FLAGS = [
 # Per-file extra flags.  The MaxSim kernels take inputs that are finite by contract (the header
 # states it), so NaN semantics need not be honoured there: without this every fmaxf of the
 # running max is preceded by two NaN-quieting self-maxes, tripling the VALU work per tile.
-FILE_FLAGS = {"maxsim.hip": ["-fno-honor-nans"]}
+FILE_FLAGS = {"maxsim.hip": ["-fno-honor-nans"], "maxsim_argmax.hip": ["-fno-honor-nans"]}
 
 
 def _compile(src, verbose):

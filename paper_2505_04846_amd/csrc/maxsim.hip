@@ -12,13 +12,10 @@
 //     last token re-load that last token, which leaves the maximum unchanged (max is
 //     idempotent), so no masking is needed.
 //   * C layout (32x32): lane l holds column l % 32 (a query slot) and the 16 rows
-//     8 (i / 4) + 4 (l / 32) + i % 4, i = 0..15 (document tokens).  The plain score folds each
-//     tile's 16 values into one running max per lane with v_max3 (8 instructions per tile and
-//     block); the argmax variant also folds them into one integer key that carries the lowest
-//     row holding the maximum (the tile keys below), and keeps the tile of the best key (the document
-//     token is kept, not the tile's values), which leaves room for three resident workgroups
-//     per CU.  At the end of a document the two half-waves are combined and the slot maxima
-//     summed per query.
+//     8 (i / 4) + 4 (l / 32) + i % 4, i = 0..15 (document tokens).  The score folds each tile's
+//     16 values into one running max per lane with v_max3 (8 instructions per tile and block).
+//     At the end of a document the two half-waves are combined and the slot maxima summed per
+//     query.  (The loss also needs the argmax token: maxsim_argmax.hip.)
 //   * Workgroup = 4 waves on 4 query sets, all consuming the same stream of document tiles,
 //     which the workgroup stages through LDS (double-buffered, one stage in flight).  Workgroups
 //     sharing a document range are mapped onto the same XCD and start together, so the range is
@@ -27,28 +24,12 @@
 //   * K permutation.  Lane half h = l / 32 of step s carries contraction indices
 //     16 s + 8 h .. 16 s + 8 h + 7 for both operands; A and B use the same rule, so every
 //     product pairs matching indices whatever order the hardware reduces them in.
-#include <type_traits>
-
-#include "common.h"
-#include "kernels.h"
+#include "maxsim_common.h"
 
 namespace hpr {
+namespace msim {
 
 namespace {
-
-typedef __attribute__((ext_vector_type(16))) float f32x16;
-
-struct MaxsimArgs {
-  const uint16_t* q;
-  const uint16_t* d;
-  const int64_t* off;
-  const int64_t* part;
-  float* scores;
-  uint16_t* amax;
-  int32_t* flag;
-  int64_t n_docs, n_tok;
-  int nq, lq, lqp, qpw, dim, n_qgroups, n_ranges;
-};
 
 // LDS geometry of one 32-token tile: rows of KS*32 bytes holding 16-byte chunks at
 // XOR-swizzled positions, so that the 16 lanes of a read phase (16 different rows, one chunk
@@ -64,59 +45,6 @@ struct TileGeom {
   static constexpr int kSwz = kCpr < 16 ? kCpr - 1 : 15;
 };
 
-// Position of tile `t` of the current document stream; uniform across the workgroup.  Token
-// and document indices fit 32 bits (the host rejects stores of 2^31 tokens or more).
-struct TileCursor {
-  int d;      // document
-  int base;   // first token row (clamped)
-  int len;    // tokens (>= 1)
-  int t;      // tile index within the document
-  int cnt;    // tiles of the document
-};
-
-// Which tiles a stage holds, in scalar registers: the stage starts at tile t0 of document d0;
-// bit j of `valid` / `last` / `lng` says that tile j exists / ends its document / belongs to a
-// document of more than 65536 tokens.
-struct StageDesc {
-  int d0;
-  int t0;
-  uint32_t valid, last, lng;
-};
-
-// Argmax keys ("tile keys") of one 32x32 tile column: the lane's 16 values v_r (r = 0..15,
-// rows ascending with r) as order-preserving integers o(v) (o(v) = bits of v for v >= 0,
-// bits ^ 0x7fffffff below zero: increasing in v) with the low 4 bits replaced by 15 - r.  The
-// signed maximum of the keys is then the largest o(v) & ~15 held by the lowest row, in one
-// v_bitop3 per value ((bits & ~15) | (15 - r), truth table 0xea: a & b | c) plus one three-way
-// max per two values (a compare-and-select search of the 16 rows costs about twice as many
-// instructions).  The row selected is the first one whose value equals the maximum up to its 4
-// lowest mantissa bits (a relative window below 2^-19); the score itself takes the exact
-// maximum.  For v >= 0, o(v) = bits(v): a lane whose tile holds a non-negative value needs
-// nothing else; a lane whose 16 values are all negative (its key is then negative) redoes the
-// keys with the sign-flipped encoding, key ^ 0x7ffffff0.
-__device__ __forceinline__ int max3_i(int a, int b, int c) { return max(max(a, b), c); }
-
-// Cross-lane moves within a row of 16 lanes through DPP (no LDS round trip).
-template <int CTRL>
-__device__ __forceinline__ float dpp_f(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL,
-                                                            0xf, 0xf, false));
-}
-constexpr int kDppQuadXor1 = 0xb1;    // quad_perm [1, 0, 3, 2]
-constexpr int kDppQuadXor2 = 0x4e;    // quad_perm [2, 3, 0, 1]
-constexpr int kDppRowHalfMirror = 0x141;
-constexpr int kDppRowMirror = 0x140;
-
-// Sum over the 32 lanes l, l ^ 1, ..., of each half-wave in a fixed order; every lane of the
-// half gets the total.
-__device__ __forceinline__ float half32_sum(float v) {
-  v += dpp_f<kDppQuadXor1>(v);
-  v += dpp_f<kDppQuadXor2>(v);
-  v += dpp_f<kDppRowHalfMirror>(v);  // quad q with quad 1 - q of the same half row
-  v += dpp_f<kDppRowMirror>(v);      // the two half rows: the 16-lane row total
-  v += __shfl_xor(v, 16);            // the two rows of the half-wave
-  return v;
-}
 
 // Waves per SIMD the register allocation of the score kernel must allow: two (up to 256 VGPRs),
 // which leaves the dim-128 variant room for 128 query slots per wave (measured 7-10 % faster
@@ -378,403 +306,6 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB))) void maxsim_kerne
   }
 }
 
-// ---------------------------------------------------------------------------------------------
-// MaxSim with the argmax (the loss forward), software-pipelined.  The epilogue of a tile (the
-// running maximum, the packed argmax tile keys and their maximum) costs about half as
-// many issue cycles as the tile's MFMAs, so each wave keeps two accumulator sets: the MFMAs of
-// tile t are issued interleaved with the epilogue of tile t - 1 (sched_group_barrier pattern:
-// one A operand read per k-step, then per MFMA a few VALU instructions), and one wave keeps the
-// matrix pipe busy while it works through the previous tile's values.  Two waves per SIMD
-// (the second accumulator set needs the registers of a third resident wave).
-//
-// LDS rows are KS * 32 bytes padded by 16 (no swizzle): the A operand of k-step s sits at a
-// fixed offset 32 s from a per-lane base, so the KS reads of a tile take immediate offsets; the
-// 16 rows of a read phase start 16 bytes apart modulo the 256-byte bank width, which keeps the
-// phase conflict-free.
-//
-// Results: the per-document scores and argmax tokens of a stage are written to LDS by the
-// epilogues (the last tile of a stage finishes in the next stage), and to HBM two stages later,
-// after a barrier has passed behind every epilogue of the stage: a ring of three result buffers.
-template <int KS>
-struct ArgGeom {
-  static constexpr int kCpr = KS * 2;                  // 16-byte chunks per row
-  static constexpr int kRowB = KS * 32 + 16;           // padded row
-  static constexpr int kTileB = 32 * kRowB;
-  static constexpr int kTps = KS >= 8 ? 2 : KS == 4 ? 4 : 8;  // tiles per stage (even)
-  static constexpr int kStageB = kTps * kTileB;
-};
-
-// Workgroups of maxsim_argmax_kernel per CU: two by registers (launch bounds), fewer when two
-// stages and the result ring do not fit the CU's 160 KiB of LDS twice.
-constexpr int argmax_resident(int ks) {
-  const int tile = 32 * (ks * 32 + 16);
-  const int tps = ks >= 8 ? 2 : ks == 4 ? 4 : 8;
-  const int nb = ks == 16 ? 1 : 2;
-  const int res = 3 * tps * (4 * nb + 4 * nb * 32 * 2);
-  const int by_lds = (160 * 1024) / (2 * tps * tile + res);
-  return by_lds < 2 ? by_lds : 2;
-}
-
-// What the epilogue of a computed tile needs: its tile index within the document, whether it
-// ends the document, and where its document's results go (ring slot, tile within the stage).
-struct PendTile {
-  int t;
-  int rb;
-  int j;
-  bool last;
-};
-
-template <int KS, int NB, int WPW>
-__global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
-    MaxsimArgs a, const int64_t* __restrict__ off, const int64_t* __restrict__ part) {
-  using G = ArgGeom<KS>;
-  constexpr int kThreads = 64 * WPW;
-  constexpr int kSlotsWG = WPW * NB * 32;
-  constexpr int kTps = G::kTps;
-  __shared__ __attribute__((aligned(16))) unsigned char lds[2][G::kStageB];
-  __shared__ float res_score[3][kTps][kSlotsWG / 32];
-  __shared__ uint16_t res_amax[3][kTps][kSlotsWG];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int col = lane & 31;
-  const int half = lane >> 5;
-
-  const uint32_t total = (uint32_t)a.n_qgroups * (uint32_t)a.n_ranges;
-  const uint32_t lin = (uint32_t)xcd_linear(blockIdx.x, total);
-  const int rng = __builtin_amdgcn_readfirstlane((int)(lin / (uint32_t)a.n_qgroups));
-  const int qg = __builtin_amdgcn_readfirstlane((int)(lin - (uint32_t)rng * a.n_qgroups));
-  const int d_begin = __builtin_amdgcn_readfirstlane((int)part[rng]);
-  const int d_end = __builtin_amdgcn_readfirstlane((int)part[rng + 1]);
-  if (d_begin >= d_end) return;  // uniform for the whole workgroup
-  const int qwg = qg * WPW * a.qpw;
-  const int q0 = qwg + wave * a.qpw;
-  const bool wave_active = q0 < a.nq;
-
-  // ---- query slots -> B operands (resident)
-  bf16x8 bq[NB][KS];
-  int slot_row[NB];
-  uint32_t my_blocks = 0;
-  const int lqb = a.lqp >> 5;
-#pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    const int slot = b * 32 + col;
-    const int ql = slot / a.lqp;
-    const int i = slot - ql * a.lqp;
-    const int qq = q0 + ql;
-    const bool valid = wave_active && ql < a.qpw && qq < a.nq && i < a.lq;
-    slot_row[b] = valid ? (qq - qwg) * a.lq + i : -1;
-    if (b / lqb == lane) my_blocks |= 1u << b;
-    const uint16_t* src = a.q + (valid ? (int64_t)qq * a.lq + i : 0) * a.dim;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      const int k = 16 * s + 8 * half;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (valid && k < a.dim) v = load16(src + k);
-      bq[b][s] = as_bf16x8(v);
-    }
-  }
-  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): see maxsim_kernel
-
-  const int n_tok = (int)a.n_tok;
-  auto open_doc = [&](TileCursor& c, int dd) {  // bounds clamped as in maxsim_kernel
-    const int64_t lo64 = off[dd], hi64 = off[dd + 1];
-    const uint32_t lo_hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)lo64 >> 32));
-    const uint32_t lo_lo = __builtin_amdgcn_readfirstlane((uint32_t)lo64);
-    const uint32_t hi_hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)hi64 >> 32));
-    const uint32_t hi_lo = __builtin_amdgcn_readfirstlane((uint32_t)hi64);
-    const int lo = (lo_hi == 0u && lo_lo < (uint32_t)n_tok) ? (int)lo_lo
-                   : ((int32_t)lo_hi < 0 ? 0 : n_tok - 1);
-    int hi = (hi_hi == 0u && hi_lo <= (uint32_t)n_tok) ? (int)hi_lo
-             : ((int32_t)hi_hi < 0 ? 0 : n_tok);
-    hi = hi > lo ? hi : lo + 1;
-    c.d = dd;
-    c.base = lo;
-    c.len = hi - lo;
-    c.t = 0;
-    c.cnt = (c.len + 31) >> 5;
-  };
-
-  // ---- producer (as in maxsim_kernel, unswizzled padded rows)
-  constexpr int kRp = kThreads / G::kCpr;
-  constexpr int kPpt = kRp >= 32 ? 1 : 32 / kRp;
-  constexpr int kTpp = kRp >= 32 ? kRp / 32 : 1;
-  constexpr int kUpt = kTps * kPpt / kTpp;
-  TileCursor prod;
-  open_doc(prod, d_begin);
-  u32x4 stage_regs[kUpt];
-  const int lr = (tid / G::kCpr) & 31;
-  const int lt = __builtin_amdgcn_readfirstlane((tid / G::kCpr) >> 5);
-  const int lc = tid % G::kCpr;
-  const bool lok = 8 * lc < a.dim;
-  const uint32_t lboff = 16u * lc;
-  for (int i = tid; i < (int)(sizeof(lds) / 16); i += kThreads)
-    reinterpret_cast<u32x4*>(&lds[0][0])[i] = u32x4{0u, 0u, 0u, 0u};
-  __syncthreads();
-  const uint32_t row_bytes = 2u * (uint32_t)a.dim;
-  auto fetch_stage = [&](StageDesc& sd) {
-    sd.d0 = prod.d;
-    sd.t0 = prod.t;
-    sd.valid = sd.last = sd.lng = 0u;
-#pragma unroll
-    for (int j = 0; j < kTps; ++j) {
-      const bool ok = prod.d < d_end;
-      const int r0 = ok ? prod.base + prod.t * 32 : 0;
-      const uint32_t rmx = ok ? prod.len - prod.t * 32 - 1 : 0;
-      const char* tptr = reinterpret_cast<const char*>(a.d) + (uint64_t)(uint32_t)r0 * row_bytes;
-      if (j % kTpp == lt && lok) {
-#pragma unroll
-        for (int p = 0; p < kPpt; ++p) {
-          const uint32_t row = lr + kRp * p;
-          const uint32_t r = row < rmx ? row : rmx;
-          stage_regs[(j / kTpp) * kPpt + p] = load16(tptr + (r * row_bytes + lboff));
-        }
-      }
-      if (ok) {
-        sd.valid |= 1u << j;
-        if (prod.t + 1 == prod.cnt) sd.last |= 1u << j;
-        if (prod.len > 65536) sd.lng |= 1u << j;
-        if (++prod.t == prod.cnt) {
-          if (prod.d + 1 < d_end)
-            open_doc(prod, prod.d + 1);
-          else
-            prod.d = d_end;
-        }
-      }
-    }
-  };
-  auto store_stage = [&](int buf) {
-    if (!lok) return;
-#pragma unroll
-    for (int m = 0; m < kUpt; ++m) {
-      const int j = (m / kPpt) * kTpp + lt;
-      const uint32_t row = lr + kRp * (m % kPpt);
-      *reinterpret_cast<u32x4*>(&lds[buf][j * G::kTileB + row * G::kRowB + lboff]) = stage_regs[m];
-    }
-  };
-
-  // ---- consumer state (see maxsim_kernel): rm, bk, bt per block
-  float rm[NB];
-  int bk[NB], bt[NB];
-#pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    rm[b] = -__builtin_huge_valf();
-    bk[b] = INT32_MIN;
-    bt[b] = 0;
-  }
-  const int64_t n_entries = (int64_t)a.nq * a.lq;
-  const int n_wg_q = (a.nq - qwg) < WPW * a.qpw ? (a.nq - qwg) : WPW * a.qpw;
-  const int n_wg_e = n_wg_q * a.lq;
-  const int row_base = 4 * half;
-  const uint32_t a_lane = (uint32_t)(col * G::kRowB + half * 16);  // A operand: row col, chunk half
-
-  f32x16 accA[NB], accB[NB];
-
-  // A operand fragment of k-step s of tile j in stage buffer `buf` (immediate offset 32 s).
-  auto frag = [&](int buf, int j, int s) {
-    return as_bf16x8(*reinterpret_cast<const u32x4*>(&lds[buf][j * G::kTileB] + a_lane + 32 * s));
-  };
-  // The tile is processed in kRegions scheduling regions of kRs k-steps each (at most 4, so
-  // that only two sets of A fragments are live); region p of the epilogue covers registers
-  // [kRv p, kRv (p + 1)) of every block of Y: the tile maximum mt, the packed argmax keys k (see
-  // the tile keys above) and their maximum mk; the last region also updates the running
-  // maximum.
-  constexpr int kRs = KS / 2 < 4 ? KS / 2 : 4;
-  constexpr int kRegions = KS / kRs;
-  constexpr int kRv = 16 / kRegions;
-  auto epi_part = [&](const f32x16 (&Y)[NB], int part, float (&mt)[NB], int (&k)[NB][16],
-                      int (&mk)[NB]) {
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const int r0 = kRv * part;
-      float m = fmaxf(Y[b][r0], Y[b][r0 + 1]);
-#pragma unroll
-      for (int r = r0 + 2; r < r0 + kRv; r += 2) m = fmaxf(fmaxf(m, Y[b][r]), Y[b][r + 1]);
-#pragma unroll
-      for (int r = r0; r < r0 + kRv; ++r)
-        k[b][r] = __builtin_amdgcn_bitop3_b32(__float_as_int(Y[b][r]), ~15, 15 - r, 0xea);
-      int x = max(k[b][r0], k[b][r0 + 1]);
-#pragma unroll
-      for (int r = r0 + 2; r < r0 + kRv; r += 2) x = max3_i(x, k[b][r], k[b][r + 1]);
-      mt[b] = part == 0 ? m : fmaxf(mt[b], m);
-      mk[b] = part == 0 ? x : max(mk[b], x);
-      if (part == kRegions - 1) rm[b] = fmaxf(rm[b], mt[b]);
-    }
-  };
-  // Rest of the epilogue: lanes whose tile is all negative (one branch for every block, taken
-  // by rare waves; it recomputes the keys from Y, whose registers are live until the next
-  // step, so that the region's 16 keys per block need not stay live past it), the key update,
-  // the end of a document.
-  auto epi_finish = [&](const f32x16 (&Y)[NB], const float (&mt)[NB], int (&mk)[NB],
-                        const PendTile& p) {
-    bool neg = false;
-#pragma unroll
-    for (int b = 0; b < NB; ++b) neg |= mt[b] < 0.f;
-    if (__ballot(neg) != 0) {  // a wave-uniform branch: no exec-mask save and restore
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        int kn[16];  // sign-flipped keys: ((bits ^ 0x7fffffff) & ~15) | (15 - r)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          kn[r] = __builtin_amdgcn_bitop3_b32(__float_as_int(Y[b][r]), ~15, 15 - r, 0xea) ^
-                  0x7ffffff0;
-        int x = max(kn[0], kn[1]);
-#pragma unroll
-        for (int r = 2; r < 16; r += 2) x = max3_i(x, kn[r], kn[r + 1]);
-        mk[b] = mt[b] < 0.f ? x : mk[b];
-      }
-    }
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      // strictly larger truncated key <=> mk > (bk | 15): the earlier tile keeps ties
-      const bool take = mk[b] > (bk[b] | 15);
-      bk[b] = take ? mk[b] : bk[b];
-      bt[b] = take ? p.t : bt[b];
-    }
-    if (p.last) {
-      float qs = 0.f;
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const float m = fmaxf(rm[b], __shfl_xor(rm[b], 32));
-        rm[b] = -__builtin_huge_valf();
-        const int r = (bk[b] & 15) ^ 15;
-        int x = bt[b] * 32 + row_base + r + (r & 12);  // row 8 (r / 4) + 4 half + r % 4
-        int tv = bk[b] & ~15;
-        const int otv = __shfl_xor(tv, 32);
-        const int ox = __shfl_xor(x, 32);
-        const bool tk = (otv > tv) | ((otv == tv) & (ox < x));
-        x = tk ? ox : x;
-        if (half == 0 && slot_row[b] >= 0) res_amax[p.rb][p.j][slot_row[b]] = (uint16_t)x;
-        bk[b] = INT32_MIN;
-        const float v = half32_sum(slot_row[b] >= 0 ? m : 0.f);
-        if ((my_blocks >> b) & 1u) qs += v;
-      }
-      if (lane < a.qpw) res_score[p.rb][p.j][wave * a.qpw + lane] = qs;
-    }
-  };
-  // One pipelined step: the MFMAs of tile j (stage buffer `buf`) into X and, when HAS_Y, the
-  // epilogue values of the previous tile Y interleaved with them.  Region p first issues the
-  // LDS reads of the A fragments of region p + 1 (for the last region: region 0 of tile j + 1,
-  // when that tile is in the same stage), then runs its MFMAs with a share of the epilogue's
-  // VALU instructions after each; fr[p % 2] holds the fragments region p uses (fr[0] holds tile
-  // j's region 0 on entry, tile j + 1's on exit).
-  auto step = [&](auto has_y, f32x16 (&X)[NB], const f32x16 (&Y)[NB], int buf, int j,
-                  bf16x8 (&fr)[2][kRs], float (&mt)[NB], int (&k)[NB][16], int (&mk)[NB]) {
-    constexpr bool kHasY = decltype(has_y)::value;
-    constexpr int kV = (kRv * 2 * NB + kRs * NB - 1) / (kRs * NB);  // VALU per MFMA
-#pragma unroll
-    for (int p = 0; p < kRegions; ++p) {
-      const bool last_region = p + 1 == kRegions;
-      const bool reads = !last_region || j + 1 < kTps;
-#pragma unroll
-      for (int s = 0; s < kRs; ++s) {
-        if (!last_region)
-          fr[(p + 1) & 1][s] = frag(buf, j, (p + 1) * kRs + s);
-        else if (reads)
-          fr[(p + 1) & 1][s] = frag(buf, j + 1, s);
-      }
-#pragma unroll
-      for (int s = 0; s < kRs; ++s)
-#pragma unroll
-        for (int b = 0; b < NB; ++b)
-          X[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              fr[p & 1][s], bq[b][p * kRs + s], (p == 0 && s == 0) ? f32x16{} : X[b], 0, 0, 0);
-      if constexpr (kHasY) epi_part(Y, p, mt, k, mk);
-      if (reads) __builtin_amdgcn_sched_group_barrier(0x100, kRs, 0);  // DS reads
-#pragma unroll
-      for (int i = 0; i < kRs * NB; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                // MFMA
-        if constexpr (kHasY) __builtin_amdgcn_sched_group_barrier(0x002, kV, 0);  // VALU
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  };
-
-  auto write_results = [&](const StageDesc& sd, int rb) {
-    int d = sd.d0;
-#pragma unroll 1
-    for (int j = 0; j < kTps; ++j) {
-      if (!((sd.valid >> j) & 1u)) break;
-      if ((sd.last >> j) & 1u) {
-        if (tid < n_wg_q) a.scores[(int64_t)(qwg + tid) * a.n_docs + d] = res_score[rb][j][tid];
-        uint16_t* dst = a.amax + (int64_t)d * n_entries + (int64_t)qwg * a.lq;
-        for (int e = tid; e < n_wg_e; e += kThreads) dst[e] = res_amax[rb][j][e];
-        if (((sd.lng >> j) & 1u) && tid == 0) *a.flag = 1;
-        ++d;
-      }
-    }
-  };
-
-  StageDesc cur, nxt, prv, prv2;
-  fetch_stage(cur);
-  store_stage(0);
-  __syncthreads();
-  bf16x8 fr[2][kRs];  // see step; region 0 of a stage's first tile is read after its barrier
-#pragma unroll
-  for (int s = 0; s < kRs; ++s) fr[0][s] = frag(0, 0, s);
-
-  // Pipeline state (uniform): whether a computed tile awaits its epilogue, which accumulator set
-  // holds it (B after every full stage, since kTps is even), and its descriptor.
-  bool pend = false;
-  bool pend_in_a = false;
-  PendTile pt = {0, 0, 0, false};
-  int ct = 0;  // tile index within its document of the next tile to compute
-  int stage = 0;
-  for (;; ++stage) {
-    const int buf = stage & 1;
-    const int rb = stage % 3;
-    const bool more = prod.d < d_end;
-    if (more) fetch_stage(nxt);
-    if (wave_active) {
-#pragma unroll
-      for (int j = 0; j < kTps; ++j) {
-        if (!((cur.valid >> j) & 1u)) break;  // uniform: only the final stage is partial
-        const bool last = (cur.last >> j) & 1u;
-        f32x16 (&X)[NB] = (j & 1) ? accB : accA;
-        f32x16 (&Y)[NB] = (j & 1) ? accA : accB;
-        float mt[NB];
-        int k[NB][16], mk[NB];
-        if (pend) {
-          step(std::true_type{}, X, Y, buf, j, fr, mt, k, mk);
-          epi_finish(Y, mt, mk, pt);
-        } else {
-          step(std::false_type{}, X, Y, buf, j, fr, mt, k, mk);
-        }
-        pend = true;
-        pend_in_a = !(j & 1);
-        pt = PendTile{ct, rb, j, last};
-        ct = last ? 0 : ct + 1;
-      }
-    }
-    if (stage >= 2) write_results(prv2, (stage - 2) % 3);
-    if (more) store_stage(buf ^ 1);
-    __syncthreads();
-    if (!more) break;
-#pragma unroll
-    for (int s = 0; s < kRs; ++s) fr[0][s] = frag(buf ^ 1, 0, s);
-    prv2 = prv;
-    prv = cur;
-    cur = nxt;
-  }
-  // the last computed tile's epilogue, then the results of the final two stages
-  if (wave_active && pend) {
-    float mt[NB];
-    int k[NB][16], mk[NB];
-    if (pend_in_a) {
-#pragma unroll
-      for (int p = 0; p < kRegions; ++p) epi_part(accA, p, mt, k, mk);
-      epi_finish(accA, mt, mk, pt);
-    } else {
-#pragma unroll
-      for (int p = 0; p < kRegions; ++p) epi_part(accB, p, mt, k, mk);
-      epi_finish(accB, mt, mk, pt);
-    }
-  }
-  __syncthreads();
-  if (stage >= 1) write_results(prv, (stage - 1) % 3);
-  write_results(cur, stage % 3);
-}
 
 __global__ void partition_kernel(const int64_t* off, int64_t n_docs, int64_t n_tok, int R,
                                  int64_t* part, int32_t* ctrl, int n_ctrl) {
@@ -820,28 +351,12 @@ hipError_t launch_t(const MaxsimPlan& plan, const MaxsimArgs& args, hipStream_t 
                      stream, args, args.off, args.part);
   return hipGetLastError();
 }
-template <int KS, int NB, int WPW>
-hipError_t launch_argmax_t(const MaxsimPlan& plan, const MaxsimArgs& args, hipStream_t stream) {
-  const int64_t blocks = (int64_t)plan.n_qgroups * plan.n_ranges;
-  hipLaunchKernelGGL((maxsim_argmax_kernel<KS, NB, WPW>), dim3((unsigned)blocks),
-                     dim3(64 * WPW), 0, stream, args, args.off, args.part);
-  return hipGetLastError();
-}
-
 // Variants by k-steps of 16 (dim <= 16 KS) and query blocks per wave.  Query slots per wave:
 // scores 128 (dim <= 128) or 64 (dim 256), fewer when the call has few query slots; argmax 64
 // (dim <= 128) or 32 (dim 256).
 hipError_t launch_variant(const MaxsimPlan& plan, const MaxsimArgs& args, bool argmax,
                           hipStream_t stream) {
-  if (argmax) {
-    switch (plan.ks) {
-      case 2: return launch_argmax_t<2, 2, 4>(plan, args, stream);
-      case 4: return launch_argmax_t<4, 2, 4>(plan, args, stream);
-      case 8: return launch_argmax_t<8, 2, 4>(plan, args, stream);
-      case 16: return launch_argmax_t<16, 1, 4>(plan, args, stream);
-      default: return hipErrorInvalidValue;
-    }
-  }
+  if (argmax) return launch_argmax_variant(plan, args, stream);
   switch (plan.ks * 8 + plan.nb) {
     case 2 * 8 + 1: return launch_t<2, 1, 4>(plan, args, stream);
     case 2 * 8 + 2: return launch_t<2, 2, 4>(plan, args, stream);
@@ -859,6 +374,10 @@ hipError_t launch_variant(const MaxsimPlan& plan, const MaxsimArgs& args, bool a
 }
 
 }  // namespace
+
+}  // namespace msim
+
+using namespace msim;
 
 bool maxsim_plan(int nq, int lq, int64_t n_docs, int64_t n_tok, int dim, bool argmax, int n_cu,
                  MaxsimPlan* p) {
@@ -884,7 +403,7 @@ bool maxsim_plan(int nq, int lq, int64_t n_docs, int64_t n_tok, int dim, bool ar
   // the argmax variant, whose stores are short, takes one round of resident workgroups (fewer
   // per-workgroup prologues).  No range is shorter than ~1024 tokens (the query operands are
   // re-loaded by every workgroup).
-  const int occ = argmax ? argmax_resident(p->ks) : maxsim_resident(p->ks, p->nb);
+  const int occ = argmax ? msim::argmax_resident(p->ks) : msim::maxsim_resident(p->ks, p->nb);
   const int64_t target_wg = (int64_t)(n_cu > 0 ? n_cu : 256) * occ * (argmax ? 1 : 32);
   int64_t R = (target_wg + p->n_qgroups - 1) / p->n_qgroups;
   const int64_t max_by_tokens = n_tok / 1024 > 0 ? n_tok / 1024 : 1;
