@@ -301,6 +301,56 @@ def test_loss_small_shapes(nq, lq, lens, dim, scale):
     _loss_parity(Q, D, off, pos, scale)
 
 
+@pytest.mark.parametrize("dim", [32, 128, 256])
+def test_loss_argmax_ties_go_to_the_lowest_token(dim):
+    # Bit-identical copies of one token sit in the same lane (rows 1 and 9), in the other
+    # half-wave (row 5), in later tiles (rows 33, 62) and at the document's last row (69, whose
+    # copies also fill the padding of the partial last tile).  Document 0's copies hold query
+    # token 0's and 1's maximum with a positive product; document 1's hold query token 2's and
+    # 3's maximum with every product of the document negative (the sign-flipped argmax keys).
+    # The whole subgradient must reach the lowest copy, row 1, and nothing the other copies.
+    g = torch.Generator().manual_seed(dim)
+    L = 70
+    copies = [1, 5, 9, 33, 62, 69]
+
+    def unit(x):
+        return x / x.norm(dim=-1, keepdim=True)
+
+    t0 = unit(torch.randn(dim, generator=g))
+    t1 = unit(torch.randn(dim, generator=g))
+    q = torch.stack([unit(t0 + 0.1 * torch.randn(dim, generator=g)),
+                     unit(t0 + 0.1 * torch.randn(dim, generator=g)),
+                     unit(-t1 + 0.1 * torch.randn(dim, generator=g)),
+                     unit(-t1 + 0.1 * torch.randn(dim, generator=g))])
+    # document 0: random tokens far from t0 (products with q[0], q[1] near 0)
+    d0 = unit(torch.randn(L, dim, generator=g))
+    # document 1: tokens close to -q[2], -q[3] (products near -1), and copies of a token whose
+    # products with q[2], q[3] are negative but larger
+    d1 = unit(-(q[2] + q[3])[None] + 0.05 * torch.randn(L, dim, generator=g))
+    c1 = unit(0.5 * t1 + unit(torch.randn(dim, generator=g)))
+    d2 = unit(torch.randn(L, dim, generator=g))
+    D = torch.cat([d0, d1, d2]).to(torch.bfloat16)
+    c0b, c1b = t0.to(torch.bfloat16), c1.to(torch.bfloat16)
+    for r in copies:
+        D[r] = c0b
+        D[L + r] = c1b
+    Q = q.to(torch.bfloat16)[None]
+    off = synth.csr_offsets(torch.full((3,), L, dtype=torch.int64))
+    pos = torch.tensor([2], dtype=torch.int32)
+    o = oracle.coltrast_li_loss(_bf(Q), _bf(D), off.numpy(), pos.numpy(), 1.0)
+    # the constructed maxima: document 0's copies for tokens 0, 1, document 1's for 2, 3
+    assert list(o["A"][0, :2, 0]) == [1, 1] and list(o["A"][0, 2:, 1]) == [1, 1]
+    qd = _bf(Q)[0, 2:] @ _bf(D)[L:2 * L].T  # every product behind document 1's maxima < 0
+    assert np.all(qd < 0)
+    r = hpr.coltrast_loss_fwd_bwd(*_to_dev(Q, D, off, pos), 1.0)
+    dd = r["dd"].cpu().numpy()
+    for base in (0, L):
+        assert np.any(dd[base + 1] != 0), "the lowest copy received no gradient"
+        for c in copies[1:]:
+            assert not np.any(dd[base + c] != 0), f"copy at row {c} of doc {base // L} chosen"
+    assert _rel_l2(dd, o["dD"]) <= REL and _rel_l2(r["dq"].cpu().numpy(), o["dQ"]) <= REL
+
+
 def test_loss_grads_optional_and_deterministic():
     w = synth.coltrast_step(seed=1, nq=8, n_neg=3, ld=64)
     args = _to_dev(w["Q"], w["D"], w["off"], w["pos"])
