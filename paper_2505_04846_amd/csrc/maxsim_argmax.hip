@@ -95,7 +95,7 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
       bq[b][s] = as_bf16x8(v);
     }
   }
-  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): see maxsim_kernel
+  // (the query operands are waited for together with the first stage's tiles, below)
 
   const int n_tok = (int)a.n_tok;
   auto open_doc = [&](TileCursor& c, int dd) {  // bounds clamped as in maxsim_kernel
@@ -129,9 +129,11 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
   const int lc = tid % G::kCpr;
   const bool lok = 8 * lc < a.dim;
   const uint32_t lboff = 16u * lc;
-  for (int i = tid; i < (int)(sizeof(lds) / 16); i += kThreads)
-    reinterpret_cast<u32x4*>(&lds[0][0])[i] = u32x4{0u, 0u, 0u, 0u};
-  __syncthreads();
+  if (a.dim < 16 * KS) {  // chunks past dim are never stored: they must read as zeros
+    for (int i = tid; i < (int)(sizeof(lds) / 16); i += kThreads)
+      reinterpret_cast<u32x4*>(&lds[0][0])[i] = u32x4{0u, 0u, 0u, 0u};
+    __syncthreads();
+  }
   const uint32_t row_bytes = 2u * (uint32_t)a.dim;
   auto fetch_stage = [&](StageDesc& sd) {
     sd.d0 = prod.d;
@@ -328,6 +330,10 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
 
   StageDesc cur, nxt, prv, prv2;
   fetch_stage(cur);
+  // The query operands and the first stage land together.  The operands must be resident
+  // before the pipelined loop: otherwise their pending loads make the compiler wait for every
+  // load in flight (the prefetch included) at each tile.
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
   store_stage(0);
   __syncthreads();
   bf16x8 fr[2][kRs];  // see step; region 0 of a stage's first tile is read after its barrier
