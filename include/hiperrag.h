@@ -75,7 +75,7 @@ typedef int32_t hpr_status;
  *   Top-k: 1 <= k <= min(n, 1024) (k outside that range is HPR_ERR_INVALID_ARG).
  *   coltrast_loss_fwd_bwd and coltrast_total_loss_fwd_bwd: the same lq limits, nq * lq <= 16384
  *     and every document has at most 65536 tokens (the latter is checked on the device: a
- *     longer document makes the loss NaN).
+ *     longer document scores NaN, which makes the loss NaN).
  *   dense_ip_topk: dim % 8 == 0, 8 <= dim <= 8192; n < 2^31.
  *   semantic_chunk: dim % 8 == 0, 8 <= dim <= 4096; 1 <= n < 2^31.
  */
@@ -274,13 +274,17 @@ hpr_status hpr_scale_f32(float* x, int64_t n, const float* scale, void* stream);
 /* Calibration for benchmarks: what the device sustains, to report beside the published peaks.
  *   hpr_mfma_calibration  launches a kernel of 8 waves per CU, each running `iters` iterations
  *                         of four independent v_mfma_f32_32x32x16_bf16 on register operands (no
- *                         memory traffic); *flops [host] receives its FLOP count.  sink: device
+ *                         memory traffic); *flops [host] receives its FLOP count.  operands: 0 =
+ *                         a fixed low-entropy bit pattern, 1 = random bf16 values of the size of
+ *                         unit-vector components (the matrix cores' sustained rate depends on
+ *                         the operands' bits; 1 is the ceiling for embeddings).  sink: device
  *                         fp32 [4096] scratch.  Time it on `stream` (or with
  *                         hpr_kernel_timing_read("mfma_calibration")).
  *   hpr_read_calibration  streams `bytes` (a positive multiple of 16) of device memory at `buf`
  *                         with 16-byte loads.  sink: device uint32 [16384] scratch.  Timing
  *                         name "read_calibration". */
-hpr_status hpr_mfma_calibration(int64_t iters, float* sink, double* flops, void* stream);
+hpr_status hpr_mfma_calibration(int64_t iters, int32_t operands, float* sink, double* flops,
+                                void* stream);
 hpr_status hpr_read_calibration(const void* buf, int64_t bytes, uint32_t* sink, void* stream);
 
 /* Per-kernel timing for benchmarks.  While enabled, every kernel the library launches is

@@ -71,7 +71,7 @@ _SIGNATURES = {
     "semantic_chunk": (_I32, [_P, _I64, _I32, _P, _I64, _F32, _P, _P, _P, _P, _SZ, _P]),
     "semantic_chunk_workspace_size": (_SZ, [_I64, _I32]),
     "retrieval_metrics": (_I32, [_P, _I32, _I32, _I32, _P, _P, _P, _P]),
-    "hpr_mfma_calibration": (_I32, [_I64, _P, ctypes.POINTER(ctypes.c_double), _P]),
+    "hpr_mfma_calibration": (_I32, [_I64, _I32, _P, ctypes.POINTER(ctypes.c_double), _P]),
     "hpr_read_calibration": (_I32, [_P, _I64, _P, _P]),
     "hpr_csr_validate": (_I32, [_P, _I64, _I64, _P, _P, _P]),
     "hpr_scale_f32": (_I32, [_P, _I64, _P, _P]),
@@ -377,34 +377,40 @@ def retrieval_metrics(idx, positive, k=None):
 
 
 def calibrate(device="cuda:0", mfma_iters=20000, read_bytes=16 << 30, reps=3):
-    """Measured ceilings of this device: (bf16 MFMA TFLOP/s, HBM read GB/s), each the best of
-    `reps` timed launches of the library's calibration kernels on the current stream."""
+    """Measured ceilings of this device: bf16 MFMA TFLOP/s on a fixed low-entropy operand
+    pattern and on random embedding-sized operands, and the HBM read rate in GB/s; each the
+    best of `reps` timed launches of the library's calibration kernels on the current stream."""
     dev = torch.device(device)
     L = lib()
     sink_f = torch.empty(4096, dtype=torch.float32, device=dev)
     sink_u = torch.empty(16384, dtype=torch.int32, device=dev)
     buf = torch.ones(read_bytes // 4, dtype=torch.float32, device=dev)
     flops = ctypes.c_double(0.0)
-    best_t, best_b = 0.0, 0.0
+    best = [0.0, 0.0, 0.0]
     with torch.cuda.device(dev):
         s = _stream(dev)
-        for rep in range(reps + 1):  # the first of each is a warm-up
+
+        def timed(launch):
             a = torch.cuda.Event(enable_timing=True)
             b = torch.cuda.Event(enable_timing=True)
             a.record()
-            _check(L.hpr_mfma_calibration(mfma_iters, _ptr(sink_f), ctypes.byref(flops), s))
+            launch()
             b.record()
             b.synchronize()
+            return a.elapsed_time(b) * 1e-3
+
+        for rep in range(reps + 1):  # the first of each is a warm-up
+            for operands in (0, 1):
+                t = timed(lambda: _check(L.hpr_mfma_calibration(
+                    mfma_iters, operands, _ptr(sink_f), ctypes.byref(flops), s)))
+                if rep:
+                    best[operands] = max(best[operands], flops.value / t / 1e12)
+            t = timed(lambda: _check(L.hpr_read_calibration(_ptr(buf), buf.numel() * 4,
+                                                            _ptr(sink_u), s)))
             if rep:
-                best_t = max(best_t, flops.value / (a.elapsed_time(b) * 1e-3) / 1e12)
-            a.record()
-            _check(L.hpr_read_calibration(_ptr(buf), buf.numel() * 4, _ptr(sink_u), s))
-            b.record()
-            b.synchronize()
-            if rep:
-                best_b = max(best_b, buf.numel() * 4 / (a.elapsed_time(b) * 1e-3) / 1e9)
+                best[2] = max(best[2], buf.numel() * 4 / t / 1e9)
     del buf
-    return best_t, best_b
+    return tuple(best)
 
 
 def kernel_timing(enable):

@@ -111,7 +111,7 @@ hpr_status check_lq(int32_t lq, int32_t dim, bool argmax) {
 }
 
 // Control words of the loss call: the error flag and the InfoNCE completion counter (both
-// zeroed by the partition kernel of the call).
+// zeroed by the MaxSim argmax kernel of the call).
 constexpr int kLossCtrlWords = 2;
 
 size_t part_bytes(int64_t n_docs) {
@@ -142,19 +142,22 @@ hpr_status run_maxsim(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t*
   MaxsimPlan plan;
   if (!maxsim_plan(nq, lq, n_docs, n_tok, dim, amax != nullptr, n_cu, &plan))
     return fail(HPR_ERR_UNSUPPORTED_SHAPE, "no MaxSim plan for this shape");
-  hipError_t e = timed("partition", stream, [&] {
-    return launch_partition(d_off, n_docs, n_tok, plan.n_ranges, part, ctrl, n_ctrl, stream);
-  });
-  if (e != hipSuccess) return hip_fail(e, "partition launch");
+  hipError_t e = hipSuccess;
+  if (!amax) {  // the argmax kernel finds its own ranges (one round of workgroups)
+    e = timed("partition", stream, [&] {
+      return launch_partition(d_off, n_docs, n_tok, plan.n_ranges, part, ctrl, n_ctrl, stream);
+    });
+    if (e != hipSuccess) return hip_fail(e, "partition launch");
+  }
   e = timed(amax ? "maxsim_argmax" : "maxsim", stream, [&] {
     return launch_maxsim(plan, q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, part, scores, amax,
-                         ctrl, stream);
+                         ctrl, n_ctrl, stream);
   });
   if (e != hipSuccess) return hip_fail(e, "maxsim launch");
   return HPR_OK;
 }
 
-// Workspace of the loss calls: S, G, the argmax table, the partition, control words, loss
+// Workspace of the loss calls: S, G, the argmax table, control words, loss
 // terms and dQ partial sums; with the contrastive half also the pooled rows and their norms,
 // dL_C/dc, its terms and the per-query / per-document gradient parts.
 size_t loss_ws_bytes(int32_t nq, int32_t lq, int64_t n_docs, int64_t n_tok, int32_t dim,
@@ -165,7 +168,7 @@ size_t loss_ws_bytes(int32_t nq, int32_t lq, int64_t n_docs, int64_t n_tok, int3
   const int64_t E = (int64_t)nq * lq;
   const size_t gq = align_up((size_t)grad_q_ranges(n_docs, n_tok, E, dim) * (size_t)E *
                              (size_t)dim * sizeof(float));
-  size_t b = 2 * sd + am + part_bytes(n_docs) + align_up((size_t)kLossCtrlWords * sizeof(int32_t)) +
+  size_t b = 2 * sd + am + align_up((size_t)kLossCtrlWords * sizeof(int32_t)) +
              align_up((size_t)nq * sizeof(float)) + gq;
   if (contrastive) {
     const size_t qd = align_up((size_t)nq * (size_t)dim * sizeof(float));
@@ -201,13 +204,12 @@ hpr_status run_loss(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d
   float* S = c.take<float>((size_t)nq * n_docs * sizeof(float));
   float* G = c.take<float>((size_t)nq * n_docs * sizeof(float));
   uint16_t* amax = c.take<uint16_t>((size_t)n_docs * nq * lq * sizeof(uint16_t));
-  int64_t* part = c.take<int64_t>(part_bytes(n_docs));
   const int n_ctrl = kLossCtrlWords;
   int32_t* ctrl = c.take<int32_t>((size_t)n_ctrl * sizeof(int32_t));
   float* terms = c.take<float>((size_t)nq * sizeof(float));
   float* gq_part = c.take<float>((size_t)grad_q_ranges(n_docs, n_tok, (int64_t)nq * lq, dim) *
                                  (size_t)nq * lq * dim * sizeof(float));
-  st = run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, S, amax, ctrl, n_ctrl, part, s);
+  st = run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, S, amax, ctrl, n_ctrl, nullptr, s);
   if (st != HPR_OK) return st;
   const float w = total ? 0.5f : 1.0f;
   hipError_t e = timed("infonce", s, [&] {
@@ -403,8 +405,11 @@ hpr_status retrieval_metrics(const int64_t* topk_idx, int32_t nq, int32_t ld, in
   return e == hipSuccess ? HPR_OK : hip_fail(e, "retrieval metrics launch");
 }
 
-hpr_status hpr_mfma_calibration(int64_t iters, float* sink, double* flops, void* stream) {
+hpr_status hpr_mfma_calibration(int64_t iters, int32_t operands, float* sink, double* flops,
+                                void* stream) {
   if (!sink || !flops) return fail(HPR_ERR_INVALID_ARG, "sink and flops must be non-NULL");
+  if (operands != 0 && operands != 1)
+    return fail(HPR_ERR_INVALID_ARG, "operands (%d) must be 0 or 1", operands);
   if (iters < 1 || iters > (int64_t(1) << 32))
     return fail(HPR_ERR_INVALID_ARG, "iters (%lld) must be in [1, 2^32]", (long long)iters);
   int n_cu = 0;
@@ -412,7 +417,8 @@ hpr_status hpr_mfma_calibration(int64_t iters, float* sink, double* flops, void*
   if (st != HPR_OK) return st;
   *flops = (double)mfma_calibration_waves(n_cu) * (double)iters * 4.0 * 32768.0;
   hipError_t e = timed("mfma_calibration", static_cast<hipStream_t>(stream), [&] {
-    return launch_mfma_calibration(sink, iters, n_cu, static_cast<hipStream_t>(stream));
+    return launch_mfma_calibration(sink, iters, n_cu, operands == 1,
+                                   static_cast<hipStream_t>(stream));
   });
   return e == hipSuccess ? HPR_OK : hip_fail(e, "MFMA calibration launch");
 }

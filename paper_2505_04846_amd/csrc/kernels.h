@@ -28,18 +28,20 @@ struct MaxsimPlan {
 bool maxsim_plan(int nq, int lq, int64_t n_docs, int64_t n_tok, int dim, bool argmax, int n_cu,
                  MaxsimPlan* plan);
 
-// part[r], r = 0..R: first document of range r (token-balanced, documents never split).
-// Also zeroes ctrl[0 .. n_ctrl) (if ctrl is non-null): the error flag and the completion
-// counters used by later kernels of the same call.
+// part[r], r = 0..R: first document of range r (token-balanced, documents never split), the
+// range table of the score kernel.  Also zeroes ctrl[0 .. n_ctrl) (if ctrl is non-null).
 hipError_t launch_partition(const int64_t* off, int64_t n_docs, int64_t n_tok, int n_ranges,
                             int64_t* part, int32_t* ctrl, int n_ctrl, hipStream_t stream);
 
 // MaxSim scores (and, when amax != nullptr, the lowest-index argmax token per (q, i, d), stored
-// as uint16 [n_docs, nq * lq]; a document longer than 65536 tokens raises *flag).
+// as uint16 [n_docs, nq * lq]).  Without amax the kernel reads the range table `part` of
+// launch_partition.  With amax it finds its ranges itself (part is not read), zeroes
+// ctrl[0 .. n_ctrl) (the control words of the later kernels of the call; ctrl may be null), and
+// scores a document longer than 65536 tokens as NaN.
 hipError_t launch_maxsim(const MaxsimPlan& plan, const uint16_t* q, int nq, int lq,
                          const uint16_t* d_tok, const int64_t* off, int64_t n_docs,
                          int64_t n_tok, int dim, const int64_t* part, float* scores,
-                         uint16_t* amax, int32_t* flag, hipStream_t stream);
+                         uint16_t* amax, int32_t* ctrl, int n_ctrl, hipStream_t stream);
 
 // CSR validation: writes the lowest offending (doc * 2 + is_empty) into *bad (uint64, ~0 = ok).
 hipError_t launch_csr_validate(const int64_t* off, int64_t n_docs, int64_t n_tok,
@@ -159,7 +161,8 @@ hipError_t launch_retrieval_metrics(const int64_t* idx, int nq, int64_t ld, int 
 // 4-wave workgroup); a pure streaming read of `bytes` (a multiple of 16) with `blocks`
 // workgroups (sink: one word per workgroup).
 int64_t mfma_calibration_waves(int n_cu);
-hipError_t launch_mfma_calibration(float* sink, int64_t iters, int n_cu, hipStream_t stream);
+hipError_t launch_mfma_calibration(float* sink, int64_t iters, int n_cu, bool random_operands,
+                                   hipStream_t stream);
 hipError_t launch_read_calibration(const void* buf, int64_t bytes, uint32_t* sink, int blocks,
                                    hipStream_t stream);
 

@@ -428,7 +428,7 @@ hipError_t launch_partition(const int64_t* off, int64_t n_docs, int64_t n_tok, i
 hipError_t launch_maxsim(const MaxsimPlan& plan, const uint16_t* q, int nq, int lq,
                          const uint16_t* d_tok, const int64_t* off, int64_t n_docs,
                          int64_t n_tok, int dim, const int64_t* part, float* scores,
-                         uint16_t* amax, int32_t* flag, hipStream_t stream) {
+                         uint16_t* amax, int32_t* ctrl, int n_ctrl, hipStream_t stream) {
   MaxsimArgs args;
   args.q = q;
   args.d = d_tok;
@@ -436,7 +436,8 @@ hipError_t launch_maxsim(const MaxsimPlan& plan, const uint16_t* q, int nq, int 
   args.part = part;
   args.scores = scores;
   args.amax = amax;
-  args.flag = flag;
+  args.ctrl = ctrl;
+  args.n_ctrl = ctrl != nullptr ? n_ctrl : 0;
   args.n_docs = n_docs;
   args.n_tok = n_tok;
   args.nq = nq;

@@ -44,9 +44,45 @@ struct PendTile {
   bool last;
 };
 
+// First document of token range r out of R equal ranges: the least d in [0, n_docs) with
+// off[d] >= floor(n_tok * r / R), or n_docs when there is none or r = R (documents are never
+// split; a range can be empty).  Lanes 0-31 answer for r = r0 and lanes 32-63 for r0 + 1, each
+// half by a 32-way search that keeps the answer inside [lo, hi]: a round probes the last offset
+// of each of 32 equal slices of [lo, hi); the probes below the target form a prefix (offsets
+// ascend), and its length picks the slice that holds the answer.  A span S shrinks to at most
+// ceil(S / 32) - 1 per round: two rounds for 1024 documents, four for 10^6.  Whatever the
+// offsets hold, lo stays within [0, n_docs] and every probe within [0, n_docs).
+__device__ int range_first_doc(const int64_t* __restrict__ off, int64_t n_docs, int64_t n_tok,
+                               int R, int r0, int lane) {
+  const int half = lane >> 5, i = lane & 31;
+  // floor(n_tok * r / R) in 32 bits: n_tok < 2^31 and R <= 2^16, so (n_tok % R) * r < 2^32
+  const uint32_t nt = (uint32_t)n_tok, ru = (uint32_t)R, qt = nt / ru, mt = nt % ru;
+  const uint32_t r = (uint32_t)r0 + (uint32_t)half;
+  const uint32_t t0 = qt * (uint32_t)r0 + mt * (uint32_t)r0 / ru;
+  const uint32_t t1 = qt * (uint32_t)(r0 + 1) + mt * (uint32_t)(r0 + 1) / ru;
+  const int64_t target = half ? t1 : t0;
+  int64_t lo = r >= ru ? n_docs : 0, hi = n_docs;
+  while (__ballot(lo < hi)) {
+    const bool open = lo < hi;
+    const int64_t step = (hi - lo + 31) >> 5;
+    const int64_t last = hi - 1;
+    int64_t p = lo + (int64_t)(i + 1) * step - 1;
+    p = p < last ? p : last;
+    const bool below = open && off[p] < target;
+    const int c = __popc((uint32_t)(__ballot(below) >> (32 * half)));
+    if (open) {
+      const int64_t pl = lo + (int64_t)c * step - 1, ph = pl + step;
+      const int64_t nlo = c > 0 ? (pl < last ? pl : last) + 1 : lo;
+      hi = c < 32 ? (ph < last ? ph : last) : hi;
+      lo = nlo;
+    }
+  }
+  return (int)lo;
+}
+
 template <int KS, int NB, int WPW>
 __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
-    MaxsimArgs a, const int64_t* __restrict__ off, const int64_t* __restrict__ part) {
+    MaxsimArgs a, const int64_t* __restrict__ off) {
   using G = ArgGeom<KS>;
   constexpr int kThreads = 64 * WPW;
   constexpr int kSlotsWG = WPW * NB * 32;
@@ -65,9 +101,7 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
   const uint32_t lin = (uint32_t)xcd_linear(blockIdx.x, total);
   const int rng = __builtin_amdgcn_readfirstlane((int)(lin / (uint32_t)a.n_qgroups));
   const int qg = __builtin_amdgcn_readfirstlane((int)(lin - (uint32_t)rng * a.n_qgroups));
-  const int d_begin = __builtin_amdgcn_readfirstlane((int)part[rng]);
-  const int d_end = __builtin_amdgcn_readfirstlane((int)part[rng + 1]);
-  if (d_begin >= d_end) return;  // uniform for the whole workgroup
+  if (blockIdx.x == 0 && tid < a.n_ctrl) a.ctrl[tid] = 0;  // read only by later kernels
   const int qwg = qg * WPW * a.qpw;
   const int q0 = qwg + wave * a.qpw;
   const bool wave_active = q0 < a.nq;
@@ -96,6 +130,12 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
     }
   }
   // (the query operands are waited for together with the first stage's tiles, below)
+
+  // ---- this workgroup's documents: found while the query loads are in flight
+  const int first = range_first_doc(off, a.n_docs, a.n_tok, a.n_ranges, rng, lane);
+  const int d_begin = __builtin_amdgcn_readlane(first, 0);
+  const int d_end = __builtin_amdgcn_readlane(first, 32);
+  if (d_begin >= d_end) return;  // uniform for the whole workgroup
 
   const int n_tok = (int)a.n_tok;
   auto open_doc = [&](TileCursor& c, int dd) {  // bounds clamped as in maxsim_kernel
@@ -319,10 +359,13 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
     for (int j = 0; j < kTps; ++j) {
       if (!((sd.valid >> j) & 1u)) break;
       if ((sd.last >> j) & 1u) {
-        if (tid < n_wg_q) a.scores[(int64_t)(qwg + tid) * a.n_docs + d] = res_score[rb][j][tid];
+        // a document too long for 16-bit argmax offsets scores NaN, which the loss carries on
+        const bool lng = (sd.lng >> j) & 1u;
+        if (tid < n_wg_q)
+          a.scores[(int64_t)(qwg + tid) * a.n_docs + d] =
+              lng ? __builtin_nanf("") : res_score[rb][j][tid];
         uint16_t* dst = a.amax + (int64_t)d * n_entries + (int64_t)qwg * a.lq;
         for (int e = tid; e < n_wg_e; e += kThreads) dst[e] = res_amax[rb][j][e];
-        if (((sd.lng >> j) & 1u) && tid == 0) *a.flag = 1;
         ++d;
       }
     }
@@ -406,7 +449,7 @@ template <int KS, int NB, int WPW>
 hipError_t launch_argmax_t(const MaxsimPlan& plan, const MaxsimArgs& args, hipStream_t stream) {
   const int64_t blocks = (int64_t)plan.n_qgroups * plan.n_ranges;
   hipLaunchKernelGGL((maxsim_argmax_kernel<KS, NB, WPW>), dim3((unsigned)blocks),
-                     dim3(64 * WPW), 0, stream, args, args.off, args.part);
+                     dim3(64 * WPW), 0, stream, args, args.off);
   return hipGetLastError();
 }
 

@@ -16,12 +16,12 @@ struct MaxsimArgs {
   const uint16_t* q;
   const uint16_t* d;
   const int64_t* off;
-  const int64_t* part;
+  const int64_t* part;  // range table of the score kernel (the argmax kernel finds its own)
   float* scores;
   uint16_t* amax;
-  int32_t* flag;
+  int32_t* ctrl;        // argmax kernel: control words of the call, zeroed by workgroup 0
   int64_t n_docs, n_tok;
-  int nq, lq, lqp, qpw, dim, n_qgroups, n_ranges;
+  int nq, lq, lqp, qpw, dim, n_qgroups, n_ranges, n_ctrl;
 };
 
 // Position of tile `t` of the current document stream; uniform across the workgroup.  Token

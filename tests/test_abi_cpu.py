@@ -170,9 +170,11 @@ def test_retrieval_metrics_rejects():
 def test_calibration_rejects_bad_arguments():
     lib = hpr.lib()
     flops = ctypes.c_double(0)
-    assert lib.hpr_mfma_calibration(0, FAKE, ctypes.byref(flops), NULL) == 1
-    assert lib.hpr_mfma_calibration(10, NULL, ctypes.byref(flops), NULL) == 1
-    assert lib.hpr_mfma_calibration(10, FAKE, None, NULL) == 1
+    assert lib.hpr_mfma_calibration(0, 0, FAKE, ctypes.byref(flops), NULL) == 1
+    assert lib.hpr_mfma_calibration(10, 2, FAKE, ctypes.byref(flops), NULL) == 1
+    assert lib.hpr_mfma_calibration(10, -1, FAKE, ctypes.byref(flops), NULL) == 1
+    assert lib.hpr_mfma_calibration(10, 1, NULL, ctypes.byref(flops), NULL) == 1
+    assert lib.hpr_mfma_calibration(10, 0, FAKE, None, NULL) == 1
     assert lib.hpr_read_calibration(NULL, 1024, FAKE, NULL) == 1
     assert lib.hpr_read_calibration(FAKE, 1000, FAKE, NULL) == 1
     assert lib.hpr_read_calibration(FAKE_ODD, 1024, FAKE, NULL) == 1

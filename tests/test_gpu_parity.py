@@ -351,6 +351,34 @@ def test_loss_argmax_ties_go_to_the_lowest_token(dim):
     assert _rel_l2(dd, o["dD"]) <= REL and _rel_l2(r["dq"].cpu().numpy(), o["dQ"]) <= REL
 
 
+def test_loss_ranges_inside_a_long_document_and_over_many_tiny_ones():
+    # The argmax kernel splits the tokens into equal ranges and each workgroup searches the
+    # offsets for the documents that start in its range.  A 20,000-token document among short
+    # ones leaves ~18 of 28 ranges without a document; 20,000 documents of one or two tokens
+    # take three rounds of the search.
+    g = np.random.default_rng(7)
+    lens_a = g.integers(1, 300, 30).tolist() + [20_000] + g.integers(1, 300, 30).tolist()
+    lens_b = g.integers(1, 3, 20_000).tolist()
+    for seed, lens in ((1, lens_a), (2, lens_b)):
+        Q, D, off = _ragged(seed, 2, 32, lens, 64)
+        pos = torch.tensor([0, len(lens) - 1], dtype=torch.int32)
+        _loss_parity(Q, D, off, pos, 2.0)
+
+
+def test_loss_document_length_limit():
+    # 65,536 tokens is the longest document whose argmax offsets fit 16 bits: such a document
+    # is scored exactly; one token more and its scores, and hence the loss, are NaN.
+    Q, D, off = _ragged(3, 2, 4, [10, 65_536, 10], 8)
+    pos = torch.tensor([0, 2], dtype=torch.int32)
+    _loss_parity(Q, D, off, pos, 1.0)
+    Q, D, off = _ragged(4, 2, 4, [10, 65_537, 10], 8)
+    r = hpr.coltrast_loss_fwd_bwd(*_to_dev(Q, D, off, pos), 1.0, return_scores=True)
+    s = r["scores"].cpu().numpy()
+    assert np.all(np.isnan(s[:, 1])) and math.isnan(float(r["loss"].item()))
+    o = oracle.maxsim_scores(_bf(Q), _bf(D), off.numpy())
+    _assert_close(s[:, [0, 2]], o[:, [0, 2]], rel=1e-4, what="scores")
+
+
 def test_loss_grads_optional_and_deterministic():
     w = synth.coltrast_step(seed=1, nq=8, n_neg=3, ld=64)
     args = _to_dev(w["Q"], w["D"], w["off"], w["pos"])
