@@ -333,10 +333,10 @@ def main():
         del src, dst
     # what this device sustains, measured, beside the published peaks: a pure-MFMA kernel
     # (bf16 32x32x16 chains on registers; fp16 runs at the same rate) on a fixed low-entropy
-    # operand pattern and on random embedding-sized operands, and a pure streaming read.  The
-    # matrix cores hold a lower clock on random operands; that rate is the MFMA kernels'
-    # measured ceiling, since their inputs are embeddings.
-    meas_fixed, meas_tflops, meas_gbs = hpr.calibrate(dev)
+    # operand pattern and on random embedding-sized operands, and a pure streaming read.  Over
+    # milliseconds of random operands the chip holds a lower clock; the higher (fixed-pattern)
+    # rate is the ceiling the rooflines quote, the other is reported beside it.
+    meas_tflops, meas_random, meas_gbs = hpr.calibrate(dev)
     W = build_workload(args.workload, dev, args.logit_scale, args.temperature, args.nq)
     print(f"[bench] workload {args.workload} ready", file=sys.stderr, flush=True)
 
@@ -417,7 +417,6 @@ def main():
             "traffic": committed_traffic(kname, twl, W["sha"]),
             "flops_per_launch": W["flops"], "avg_launch_us": kernels[kname]["avg_us"],
             "measured_peak": round(meas_tflops, 1),
-            "measured_peak_operands": "random bf16",
             "frac_of_measured": round(achieved / meas_tflops, 4),
         }
 
@@ -465,8 +464,8 @@ def main():
         "roofline_topk": roofline_topk,
         "cpu_baseline": cpu,
         "retrieval_metrics": extra,
-        "measured_peaks": {"mfma_bf16_tflops_random_operands": round(meas_tflops, 1),
-                           "mfma_bf16_tflops_fixed_operands": round(meas_fixed, 1),
+        "measured_peaks": {"mfma_bf16_tflops": round(meas_tflops, 1),
+                           "mfma_bf16_tflops_random_operands": round(meas_random, 1),
                            "hbm_read_gbs": round(meas_gbs, 1)},
         "kernels": kernels,
         "eager": {"ms_per_step": ms, "value": W["pairs"] / (ms * 1e-3)},
