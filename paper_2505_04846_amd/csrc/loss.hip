@@ -138,6 +138,7 @@ __global__ __launch_bounds__(kRowThreads) void infonce_kernel(const float* __res
 constexpr int kGqWaves = 4;
 constexpr int kGqThreads = 64 * kGqWaves;
 constexpr int kGqEntries = 4 * kGqWaves;  // (q, i) entries per workgroup: 16 lanes each
+constexpr int kGqBatch = 4;               // documents whose rows a lane gathers at once
 
 // dQ, first pass: workgroup (r, g) sums, for the 16 entries e = q * lq + i of group g, the
 // gathered rows G[q,d] * D[token a(q,i,d)] over the documents of range r.  Ranges are placed on
@@ -145,7 +146,7 @@ constexpr int kGqEntries = 4 * kGqWaves;  // (q, i) entries per workgroup: 16 la
 // 8 columns at 8 * ((lane & 15) + 16 cc).  Partials part[r][e][:] are summed by the second pass
 // in range order, so the result does not depend on scheduling.
 template <int CPL>
-__global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
+__global__ __launch_bounds__(kGqThreads, CPL == 1 ? 8 : 4) void grad_q_part_kernel(
     const uint16_t* __restrict__ D, const int64_t* __restrict__ off, int64_t n_docs,
     int64_t n_tok, int dim, int nq, int lq, const uint16_t* __restrict__ amax,
     const float* __restrict__ G, float* __restrict__ part, float* __restrict__ dq, int n_groups,
@@ -170,8 +171,10 @@ __global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
   // Documents in chunks of 32.  First, lane l loads the row index and weight of two of the
   // wave's four entries (2 (l >> 5) and the next) against document l & 31 of the chunk -- one
   // round trip for the chunk's metadata -- into the wave's table in LDS; then each 16-lane
-  // group gathers its entry's rows, 16 documents at a time, reading each document's (row,
-  // weight) with one LDS load that the group's lanes share.  Only the wave itself reads its
+  // group gathers its entry's rows, kGqBatch documents at a time, reading each document's (row,
+  // weight) with one LDS load that the group's lanes share.  Small batches keep the kernel
+  // within 64 VGPRs at dim <= 128: eight waves per SIMD, so every workgroup of the training
+  // step is resident at once.  Only the wave itself reads its
   // table, and a wave's LDS accesses complete in order.
   __shared__ int2 meta[kGqWaves][4][32];
   const int mu = lane & 31, mh = lane >> 5;
@@ -194,13 +197,13 @@ __global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
     }
     __builtin_amdgcn_wave_barrier();
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      if (db + 16 * half >= d1) break;  // uniform
-      u32x4 w[16][CPL];
-      float g[16];
+    for (int part = 0; part < 32 / kGqBatch; ++part) {
+      if (db + kGqBatch * part >= d1) break;  // uniform
+      u32x4 w[kGqBatch][CPL];
+      float g[kGqBatch];
 #pragma unroll
-      for (int uu = 0; uu < 16; ++uu) {
-        const int2 mt = meta[wave][k][16 * half + uu];
+      for (int uu = 0; uu < kGqBatch; ++uu) {
+        const int2 mt = meta[wave][k][kGqBatch * part + uu];
         const int64_t row = mt.x;
         g[uu] = __int_as_float(mt.y);
 #pragma unroll
@@ -210,7 +213,7 @@ __global__ __launch_bounds__(kGqThreads) void grad_q_part_kernel(
         }
       }
 #pragma unroll
-      for (int uu = 0; uu < 16; ++uu)
+      for (int uu = 0; uu < kGqBatch; ++uu)
 #pragma unroll
         for (int cc = 0; cc < CPL; ++cc) {
           acc[cc][0] += g[uu] * bf16_lo(w[uu][cc].x);
