@@ -279,15 +279,13 @@ __global__ void grad_q_reduce_kernel(const float* __restrict__ part, int R, int6
   grad_q_sum_ranges(part, R, i0, i1, n4, dq, dqc, lq, dim);
 }
 
-constexpr int kGdThreads = 256;
-constexpr int kGdWaves = kGdThreads / 64;
 constexpr int kGdRows = 512;        // rows of a document sorted per pass
-constexpr int kGdBatch = 8;         // positions whose Q rows a group has in flight (x2)
 constexpr int kGdMaxStageQ = 4096;  // G[:, d] is staged in LDS when nq is at most this
 
 // TPE threads read one Q row, CPT chunks of 16 bytes (8 columns) each: chunk c + TPE i of the
-// row belongs to thread c of its group (dim <= 8 TPE CPT); kGdThreads / TPE groups.  Fewer,
-// wider threads per entry spread the per-position bookkeeping over more columns.
+// row belongs to thread c of its group (dim <= 8 TPE CPT); an NT-thread workgroup has NT / TPE
+// groups.  Fewer, wider threads per entry spread the per-position bookkeeping over more
+// columns.
 __host__ __device__ inline int gd_cpt(int dim) { return dim <= 64 ? 1 : dim <= 128 ? 2 : 4; }
 __host__ __device__ inline int gd_tpe(int dim) { return 8; }
 
@@ -295,13 +293,13 @@ __host__ __device__ inline int gd_tpe(int dim) { return 8; }
 struct GdLds {
   int keys, sorted, weight, cnt, rs, gcol, total;
 };
-__host__ __device__ inline GdLds gd_lds(int E, int nq) {
+__host__ __device__ inline GdLds gd_lds(int E, int nq, int waves) {
   GdLds l;
   l.keys = 0;  // the document's argmax entries, staged once
   l.sorted = (2 * E + 15) / 16 * 16;
   l.weight = l.sorted + 4 * E;
   l.cnt = l.weight + 4 * E;
-  l.rs = l.cnt + kGdWaves * kGdRows * 4;
+  l.rs = l.cnt + waves * kGdRows * 4;  // per-wave histograms
   l.gcol = l.rs + ((kGdRows + 1) * 4 + 15) / 16 * 16;
   l.total = l.gcol + (nq <= kGdMaxStageQ ? (4 * nq + 15) / 16 * 16 : 0);
   return l;
@@ -317,19 +315,19 @@ __host__ __device__ inline GdLds gd_lds(int E, int nq) {
 //      boundaries, each slice holding about the same number of entries (a row never
 //      straddles two slices);
 //   3. each group walks its slice in order, gathering whole 256-byte Q rows (TPE x 16 bytes,
-//      straight from L2) kGdBatch positions ahead of the ones it adds, and writes each row once
+//      straight from L2) a batch of positions ahead of the ones it adds, and writes each row once
 //      it is complete -- zeros (or the contrastive part) for rows nobody selected.
 // Deterministic: every row sums its entries in entry order, with no atomics on floats.
-template <int TPE, int CPT>
-__global__ __launch_bounds__(kGdThreads, 2) void grad_d_kernel(
+template <int TPE, int CPT, int NT>
+__global__ __launch_bounds__(NT, NT >= 512 ? 4 : 2) void grad_d_kernel(
     const uint16_t* __restrict__ Q, const int64_t* __restrict__ off, int64_t n_docs,
     int64_t n_tok, int dim, int nq, int lq, uint64_t lq_magic,
     const uint16_t* __restrict__ amax, const float* __restrict__ G, float* __restrict__ dd,
     const float* __restrict__ dq_part, int dq_R, float* __restrict__ dq,
     const float* __restrict__ dqc, const float* __restrict__ ddc) {
   extern __shared__ __attribute__((aligned(16))) unsigned char gd_smem[];
-  constexpr int kGroups = kGdThreads / TPE;
-  constexpr int kRpt = kGdRows / kGdThreads;  // rows per thread in the scan
+  constexpr int kGroups = NT / TPE;
+  constexpr int kRpt = kGdRows / NT;  // rows per thread in the scan
   if (dq_part) {  // the dQ range sums, one slice per workgroup (independent of the rest)
     const int64_t n4 = (int64_t)nq * lq * dim / 4;
     const int64_t per = (n4 + gridDim.x - 1) / gridDim.x;
@@ -337,14 +335,14 @@ __global__ __launch_bounds__(kGdThreads, 2) void grad_d_kernel(
     grad_q_sum_ranges(dq_part, dq_R, i0, i0 + per < n4 ? i0 + per : n4, n4, dq, dqc, lq, dim);
   }
   const int E = nq * lq;
-  const GdLds L = gd_lds(E, nq);  // the same layout the launcher sized
+  const GdLds L = gd_lds(E, nq, NT / 64);  // the same layout the launcher sized
   uint16_t* am = reinterpret_cast<uint16_t*>(gd_smem + L.keys);
   uint32_t* spk = reinterpret_cast<uint32_t*>(gd_smem + L.sorted);
   float* sw = reinterpret_cast<float*>(gd_smem + L.weight);
   int* cnt = reinterpret_cast<int*>(gd_smem + L.cnt);
   int* rs = reinterpret_cast<int*>(gd_smem + L.rs);
   float* gcol = reinterpret_cast<float*>(gd_smem + L.gcol);
-  __shared__ int wave_tot[kGdWaves];
+  __shared__ int wave_tot[(NT / 64)];
   __shared__ int bounds[kGroups + 1];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -353,11 +351,11 @@ __global__ __launch_bounds__(kGdThreads, 2) void grad_d_kernel(
   {
     const uint16_t* src = amax + d * E;
     const int nvec = (E % 8 == 0) ? E / 8 : 0;  // 16-byte loads need 16-byte aligned rows
-    for (int i = tid; i < nvec; i += kGdThreads)
+    for (int i = tid; i < nvec; i += NT)
       reinterpret_cast<u32x4*>(am)[i] = load16(src + 8 * i);
-    for (int e = 8 * nvec + tid; e < E; e += kGdThreads) am[e] = src[e];
+    for (int e = 8 * nvec + tid; e < E; e += NT) am[e] = src[e];
     if (g_staged)
-      for (int q = tid; q < nq; q += kGdThreads) gcol[q] = G[(int64_t)q * n_docs + d];
+      for (int q = tid; q < nq; q += NT) gcol[q] = G[(int64_t)q * n_docs + d];
   }
 
   const int64_t last_tok = n_tok - 1;
@@ -366,7 +364,7 @@ __global__ __launch_bounds__(kGdThreads, 2) void grad_d_kernel(
   hi = hi <= lo ? lo + 1 : (hi > n_tok ? n_tok : hi);
   const int64_t len = hi - lo;
   // this wave's entries [eb, ee): contiguous, whole 64-entry chunks except at the end
-  const int epw = ((E + kGdWaves - 1) / kGdWaves + 63) / 64 * 64;
+  const int epw = ((E + (NT / 64) - 1) / (NT / 64) + 63) / 64 * 64;
   const int eb = wave * epw < E ? wave * epw : E;
   const int ee = eb + epw < E ? eb + epw : E;
   const uint64_t lt_mask = (1ull << lane) - 1ull;
@@ -413,7 +411,7 @@ __global__ __launch_bounds__(kGdThreads, 2) void grad_d_kernel(
         const int row = r_begin + i;
         tot[i] = 0;
         if (row < Wn)
-          for (int w = 0; w < kGdWaves; ++w) tot[i] += cnt[w * kGdRows + row];
+          for (int w = 0; w < (NT / 64); ++w) tot[i] += cnt[w * kGdRows + row];
         sum += tot[i];
       }
       int incl = sum;
@@ -433,7 +431,7 @@ __global__ __launch_bounds__(kGdThreads, 2) void grad_d_kernel(
         if (row < Wn) {
           rs[row] = run;
           int r2 = run;
-          for (int w = 0; w < kGdWaves; ++w) {
+          for (int w = 0; w < (NT / 64); ++w) {
             const int cw = cnt[w * kGdRows + row];
             cnt[w * kGdRows + row] = r2;
             r2 += cw;
@@ -441,7 +439,7 @@ __global__ __launch_bounds__(kGdThreads, 2) void grad_d_kernel(
           run += tot[i];
         }
       }
-      if (tid == kGdThreads - 1) rs[Wn] = before + incl;
+      if (tid == NT - 1) rs[Wn] = before + incl;
     }
     __syncthreads();
     // stable scatter: in entry order within the wave, ranked among equal tokens by ballots;
@@ -513,7 +511,7 @@ __global__ __launch_bounds__(kGdThreads, 2) void grad_d_kernel(
 #pragma unroll
       for (int v = 0; v < 8 * CPT; ++v) acc[v] = init[v];
       // two batches of positions in flight: the next one is loaded while this one is added
-      constexpr int kB = CPT >= 4 ? 4 : 8;  // positions per batch
+      constexpr int kB = CPT >= 4 ? 4 : NT >= 512 ? 2 : 8;  // positions per batch
       u32x4 wb[2][kB][CPT];
       float gb[2][kB];
       uint32_t rb[2][kB];
@@ -571,7 +569,7 @@ __global__ __launch_bounds__(kGdThreads, 2) void grad_d_kernel(
     }
     // rows nobody selected: their value is the document's contrastive part (or zero), one
     // thread per row
-    for (int r = tid; r < Wn; r += kGdThreads) {
+    for (int r = tid; r < Wn; r += NT) {
       if (rs[r] != rs[r + 1]) continue;
       float* dst = dd + (lo + w0 + r) * dim;
       for (int k = 0; k < dim; k += 4) {
@@ -635,21 +633,38 @@ hipError_t launch_grad_q(const uint16_t* d_tok, const int64_t* off, int64_t n_do
   return hipGetLastError();
 }
 
+template <int TPE, int CPT, int NT>
+hipError_t launch_grad_d_nt(const uint16_t* q, const int64_t* off, int64_t n_docs, int64_t n_tok,
+                           int dim, int nq, int lq, uint64_t magic, const uint16_t* amax,
+                           const float* G, float* dd, const float* dq_part, int dq_R, float* dq,
+                           const float* dqc, const float* ddc, hipStream_t stream) {
+  const int lds = gd_lds(nq * lq, nq, NT / 64).total;
+  if (lds > 65536) {  // beyond the default dynamic LDS limit (large nq * lq only)
+    const hipError_t e = hipFuncSetAttribute((const void*)grad_d_kernel<TPE, CPT, NT>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL((grad_d_kernel<TPE, CPT, NT>), dim3((unsigned)n_docs), dim3(NT), lds, stream,
+                     q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq,
+                     dqc, ddc);
+  return hipGetLastError();
+}
+
+// Up to dim 128 a document takes 8 waves (two workgroups per CU, four waves per SIMD, within
+// 128 VGPRs: two positions per gather batch) when its LDS layout still fits two workgroups per
+// CU; otherwise, and at dim 256 (whose rows need the registers), 4 waves.
 template <int TPE, int CPT>
 hipError_t launch_grad_d_t(const uint16_t* q, const int64_t* off, int64_t n_docs, int64_t n_tok,
                            int dim, int nq, int lq, uint64_t magic, const uint16_t* amax,
                            const float* G, float* dd, const float* dq_part, int dq_R, float* dq,
                            const float* dqc, const float* ddc, hipStream_t stream) {
-  const int lds = gd_lds(nq * lq, nq).total;
-  if (lds > 65536) {  // beyond the default dynamic LDS limit (large nq * lq only)
-    const hipError_t e = hipFuncSetAttribute((const void*)grad_d_kernel<TPE, CPT>,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-    if (e != hipSuccess) return e;
+  if constexpr (CPT <= 2) {
+    if (2 * gd_lds(nq * lq, nq, 8).total <= 160 * 1024)
+      return launch_grad_d_nt<TPE, CPT, 512>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G,
+                                             dd, dq_part, dq_R, dq, dqc, ddc, stream);
   }
-  hipLaunchKernelGGL((grad_d_kernel<TPE, CPT>), dim3((unsigned)n_docs), dim3(kGdThreads), lds, stream, q,
-                     off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd, dq_part, dq_R, dq, dqc,
-                     ddc);
-  return hipGetLastError();
+  return launch_grad_d_nt<TPE, CPT, 256>(q, off, n_docs, n_tok, dim, nq, lq, magic, amax, G, dd,
+                                         dq_part, dq_R, dq, dqc, ddc, stream);
 }
 
 hipError_t launch_grad_d(const uint16_t* q, const int64_t* off, int64_t n_docs, int64_t n_tok,
