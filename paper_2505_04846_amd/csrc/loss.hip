@@ -17,6 +17,7 @@ namespace hpr {
 namespace {
 
 constexpr int kRowThreads = 256;
+constexpr int kRowCache = 8;  // scores per thread kept in registers by infonce_kernel
 
 // Deterministic 256-thread block reductions (fixed tree: wave butterfly, then waves in order).
 __device__ float block_sum(float v, float* red) {
@@ -76,21 +77,39 @@ __global__ __launch_bounds__(kRowThreads) void infonce_kernel(const float* __res
   float* Gq = G + (int64_t)q * n;
   const float gscale = gw * s / (float)nq;  // gw: the loss's weight in a weighted sum
 
+  // The row's first kRowCache * kRowThreads scores stay in registers for the three passes
+  // (each later pass would otherwise be another round trip to L2); the rest are re-read.
+  float sv[kRowCache];
+#pragma unroll
+  for (int c = 0; c < kRowCache; ++c) {
+    const int64_t d = tid + (int64_t)c * kRowThreads;
+    sv[c] = d < n ? Sq[d] : 0.f;
+  }
+  // f(d, S[q, d]) for this thread's d in increasing order (static register indices first)
+  auto each = [&](auto f) {
+#pragma unroll
+    for (int c = 0; c < kRowCache; ++c) {
+      const int64_t d = tid + (int64_t)c * kRowThreads;
+      if (d < n) f(d, sv[c]);
+    }
+    for (int64_t d = tid + (int64_t)kRowCache * kRowThreads; d < n; d += kRowThreads) f(d, Sq[d]);
+  };
   float M = -__builtin_huge_valf();
   int64_t dM = n;
-  for (int64_t d = tid; d < n; d += kRowThreads) {
-    const float l = (s * Sq[d]);
+  each([&](int64_t d, float sd) {
+    const float l = (s * sd);
     if (l > M) {
       M = l;
       dM = d;
     }
-  }
+  });
   block_argmax(M, dM, redf, redi);
   // log-sum-exp = M + log1p(sum over d != dM of exp(l - M)): keeps the loss accurate when one
   // logit dominates (the loss is then ~ the small sum, which log(1 + x) would lose).
   float so = 0.f;
-  for (int64_t d = tid; d < n; d += kRowThreads)
-    if (d != dM) so += expf((s * Sq[d]) - M);
+  each([&](int64_t d, float sd) {
+    if (d != dM) so += expf((s * sd) - M);
+  });
   so = block_sum(so, redf);
   const float l1p = log1pf(so);
   const float lse = M + l1p;
@@ -105,15 +124,14 @@ __global__ __launch_bounds__(kRowThreads) void infonce_kernel(const float* __res
     // G[q,d] = (s/B) softmax; the positive gets -(s/B) * (sum of the other probabilities),
     // which equals (s/B) (p_pos - 1) without the cancellation of 1 - p_pos in fp32.
     float rest = 0.f;
-    for (int64_t d = tid; d < n; d += kRowThreads) {
-      const float sd = Sq[d];
+    each([&](int64_t d, float sd) {
       if (scores_out) scores_out[(int64_t)q * n + d] = sd;
       if (d != p) {
         const float e = expf((s * sd) - lse);
         Gq[d] = gscale * e;
         rest += e;
       }
-    }
+    });
     rest = block_sum(rest, redf);
     if (tid == 0) Gq[p] = -gscale * rest;
   }
