@@ -2,14 +2,17 @@
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
 
-Default workload: the ColTrast training step (64 queries x 32 tokens against 512 in-batch
-documents x 256 tokens, dim 128, bf16): one step = one coltrast_loss_fwd_bwd call, i.e.
-MaxSim scoring with the fused max/argmax, InfoNCE loss, and the dQ and dD gradients.
-Other workloads (--workload): coltrast_total (the same batch under the whole ColTrast loss
-(L_LI + L_C) / 2, adding mean pooling and the pooled-cosine contrastive loss), li_retrieval
-(1,024 x 32 queries against 500,000 ragged documents, exact top-100), li_large (4,096 x 64
-against 1,000,000 lognormal documents, top-1000), dense_retrieval (4,096 queries against
-10,000,000 fp16 rows of dim 4096, top-100), tiny_maxsim.
+Default workload: li_large, the largest configuration that fits one GPU: 4,096 queries x 64
+tokens against 1,000,000 documents of lognormal length (2.23e8 tokens, 57 GB of bf16, dim 128,
+10 % noisy clones), exact top-1000 per query.  One step = one maxsim_topk call over the whole
+store: MaxSim scoring with the fused max (1.5e16 FLOP), then the exact top-k select over the
+16.4 GB score matrix.
+Other workloads (--workload): coltrast_step (the training step: 64 queries x 32 tokens against
+512 in-batch documents x 256 tokens, one coltrast_loss_fwd_bwd call: MaxSim with the fused
+argmax, InfoNCE, dQ and dD), coltrast_total (the same batch under the whole ColTrast loss
+(L_LI + L_C) / 2), li_retrieval (1,024 x 32 queries against 500,000 ragged documents, exact
+top-100), dense_retrieval (4,096 queries against 10,000,000 fp16 rows of dim 4096, top-100),
+semantic_chunk, tiny_maxsim.
 
 Prints ONE JSON line.  `value` is MaxSim query x document pairs per second for the whole step
 (queries per second for dense_retrieval) with inputs resident in HBM; for the training step it
@@ -42,9 +45,11 @@ KERNELS = ("partition", "maxsim", "maxsim_argmax", "topk", "infonce", "pool", "c
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="coltrast_step",
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default 5 for li_large, 50 otherwise)")
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed warm-up steps (default 1 for li_large, 10 otherwise)")
+    ap.add_argument("--workload", default="li_large",
                     choices=["coltrast_step", "coltrast_total", "li_retrieval", "li_large",
                              "dense_retrieval", "semantic_chunk", "tiny_maxsim"])
     ap.add_argument("--logit-scale", type=float, default=1.5625,
@@ -62,7 +67,13 @@ def parse():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 256 MiB device-to-device copy three times (the "
                          "reference kernel that scales rocprofv3 FETCH_SIZE / WRITE_SIZE)")
-    return ap.parse_args()
+    a = ap.parse_args()
+    long_step = a.workload == "li_large"
+    if a.steps is None:
+        a.steps = 5 if long_step else 50
+    if a.warmup is None:
+        a.warmup = 1 if long_step else 10
+    return a
 
 
 def source_sha(*names):
@@ -80,9 +91,15 @@ def committed_traffic(kernel, workload, sha):
         return None
     with open(path) as f:
         recs = json.load(f)
+    stale = False
     for r in recs:
-        if r.get("kernel") == kernel and r.get("workload") == workload and r.get("source_sha") == sha:
-            return r.get("hbm_bytes_per_launch")
+        if r.get("kernel") == kernel and r.get("workload") == workload:
+            if r.get("source_sha") == sha:
+                return r.get("hbm_bytes_per_launch")
+            stale = True
+    if stale:
+        print(f"[bench] traffic record for {kernel} / {workload} is stale (its sources changed "
+              f"since the counters were taken): traffic reported as null", file=sys.stderr)
     return None
 
 
@@ -95,6 +112,17 @@ def blas_threads():
     except Exception:
         pass
     return len(os.sched_getaffinity(0))
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def build_workload(name, dev, scale, tau, nq_sub=None):
@@ -204,7 +232,9 @@ def build_workload(name, dev, scale, tau, nq_sub=None):
         return dict(step=step, pairs=nq * n_docs, kernel="maxsim", flops=flops, bytes=mbytes,
                     cpu_sample=cpu_sample, config=cfg, dtype="bf16", unit="pairs/s",
                     sha=source_sha("maxsim.hip", "maxsim_common.h", "common.h"),
-                    topk_bytes=4.0 * nq * n_docs + 12.0 * nq * k)
+                    topk_bytes=4.0 * nq * n_docs + 12.0 * nq * k,
+                    # seconds-long launches: a graph would save nothing and double the run
+                    graph=name == "tiny_maxsim")
 
     if name == "dense_retrieval":
         w = synth.dense_retrieval(seed=0, device=dev)
@@ -340,8 +370,14 @@ def main():
     W = build_workload(args.workload, dev, args.logit_scale, args.temperature, args.nq)
     print(f"[bench] workload {args.workload} ready", file=sys.stderr, flush=True)
 
-    for _ in range(args.warmup):
+    # Progress lines for long steps: the host waits on an event recorded after each step, in
+    # order, once every step of the timed region is enqueued (the GPU never waits on the host).
+    verbose = args.workload == "li_large"
+    for i in range(args.warmup):
         W["step"]()
+        if verbose:
+            torch.cuda.synchronize()
+            print(f"[bench] warm-up step {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
 
     hpr.kernel_timing(True)
@@ -349,11 +385,19 @@ def main():
         hpr.kernel_timing_read(name)  # drop warm-up records (timing was off; no-op)
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
+    done = [torch.cuda.Event() for _ in range(args.steps)] if verbose else []
     torch.cuda.synchronize()
+    t_host = time.perf_counter()
     start.record()
-    for _ in range(args.steps):
+    for i in range(args.steps):
         W["step"]()
+        if verbose:
+            done[i].record()
     stop.record()
+    for i, ev in enumerate(done):
+        ev.synchronize()
+        print(f"[bench] step {i + 1}/{args.steps} done ({time.perf_counter() - t_host:.1f} s)",
+              file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     hpr.kernel_timing(False)
     ms = start.elapsed_time(stop) / args.steps
@@ -439,7 +483,7 @@ def main():
     if not args.no_cpu_baseline:
         v, sample = W["cpu_sample"]()
         cpu = {"value": v, "unit": W["unit"], "cores": blas_threads(), "kind": "oracle",
-               "sample": sample}
+               "sample": sample, "cpu_model": cpu_model()}
 
     # The training step's measurement is the step captured once in a HIP graph and replayed K
     # times (every kernel of the step runs in every replay; the launch overhead of the eager

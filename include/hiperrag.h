@@ -73,8 +73,10 @@ typedef int32_t hpr_status;
  *     dim <= 256; coltrast_loss_fwd_bwd: lq <= 64 when dim <= 128, lq <= 32 when dim <= 256;
  *     n_tok < 2^31 (a store of 2^31 bf16 tokens of dim 128 would not fit one GPU's HBM).
  *   Top-k: 1 <= k <= min(n, 1024) (k outside that range is HPR_ERR_INVALID_ARG).
- *   coltrast_loss_fwd_bwd and coltrast_total_loss_fwd_bwd: the same lq limits, nq * lq <= 16384
- *     and every document has at most 65536 tokens (the latter is checked on the device: a
+ *   coltrast_loss_fwd_bwd and coltrast_total_loss_fwd_bwd: the same lq limits, nq * lq <= 16384;
+ *     with dd requested also 10 * nq * lq + 4 * nq (nq <= 4096; else 0) + 10244 <= 163840 (the
+ *     dD kernel's LDS per workgroup against a CU's 160 KiB: nq * lq up to about 15,000); and
+ *     every document has at most 65536 tokens (the latter is checked on the device: a
  *     longer document scores NaN, which makes the loss NaN).
  *   dense_ip_topk: dim % 8 == 0, 8 <= dim <= 8192; n < 2^31.
  *   semantic_chunk: dim % 8 == 0, 8 <= dim <= 4096; 1 <= n < 2^31.

@@ -267,9 +267,10 @@ class _ColTrastLI(torch.autograd.Function):
         g = grad_out.reshape(1).to(torch.float32).contiguous()
         dq = saved.pop(0) if ctx.has[0] else None
         dd = saved.pop(0) if ctx.has[1] else None
-        for t in (dq, dd):
-            if t is not None:
-                scale_(t, g)
+        # scale copies: the saved gradients stay as the forward left them, so a second backward
+        # over a retained graph scales them afresh
+        dq = scale_(dq.clone(), g) if dq is not None else None
+        dd = scale_(dd.clone(), g) if dd is not None else None
         return dq, dd, None, None, None
 
 

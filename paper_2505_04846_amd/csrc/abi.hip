@@ -194,6 +194,10 @@ hpr_status run_loss(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d
     return fail(HPR_ERR_INVALID_ARG, "logit_scale must be finite");
   if ((int64_t)nq * lq > 16384)
     return fail(HPR_ERR_UNSUPPORTED_SHAPE, "nq * lq = %lld exceeds 16384", (long long)nq * lq);
+  if (dd && grad_d_lds_bytes(nq, lq) > kMaxLdsBytes)
+    return fail(HPR_ERR_UNSUPPORTED_SHAPE,
+                "dD for nq=%d x lq=%d needs %d bytes of LDS per workgroup, above the CU's %d",
+                nq, lq, grad_d_lds_bytes(nq, lq), kMaxLdsBytes);
   if ((dq && !aligned16(dq)) || (dd && !aligned16(dd)))
     return fail(HPR_ERR_INVALID_ARG, "gradient outputs must be 16-byte aligned");
   const size_t need = loss_ws_bytes(nq, lq, n_docs, n_tok, dim, total);

@@ -72,6 +72,12 @@ hipError_t launch_grad_q(const uint16_t* d_tok, const int64_t* off, int64_t n_do
                          float* part, float* dq, bool defer_sum, const float* dqc,
                          hipStream_t stream);
 
+// LDS bytes the dD kernel needs per workgroup in its smallest (256-thread) form for nq queries
+// of lq tokens; a call whose value exceeds the CU's 160 KiB cannot run and is rejected on the
+// host (nq * lq up to about 15,000).
+constexpr int kMaxLdsBytes = 160 * 1024;
+int grad_d_lds_bytes(int nq, int lq);
+
 // dD; when dq_part is non-null it also finishes a deferred dQ (sums dq_part's ranges into dq,
 // adding dqc); ddc (optional, [n_docs][dim]) is added to every token row of its document.
 hipError_t launch_grad_d(const uint16_t* q, const int64_t* off, int64_t n_docs, int64_t n_tok,

@@ -617,6 +617,8 @@ hipError_t launch_infonce(const float* S, int nq, int64_t n_docs, const int32_t*
   return hipGetLastError();
 }
 
+int grad_d_lds_bytes(int nq, int lq) { return gd_lds(nq * lq, nq, 4).total; }
+
 int grad_q_ranges(int64_t n_docs, int64_t n_tok, int64_t E, int dim) {
   // about 2 MiB of document rows per range (an XCD's L2 holds its ranges' rows), at most 32
   // ranges and 64 MiB of partial sums

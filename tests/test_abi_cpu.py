@@ -90,6 +90,8 @@ def _loss(**kw):
     (dict(scale=float("inf")), 1), (dict(nq=1024, lq=32), 4), (dict(dq=FAKE_ODD), 1),
     (dict(lq=65), 4), (dict(lq=33, dim=256), 4),
     (dict(ws_bytes=100), 5),
+    # dD's LDS per workgroup (10 E + 4 nq + 10244 bytes) above a CU's 160 KiB
+    (dict(nq=480, lq=32, n_docs=500, n_tok=16000), 4), (dict(nq=4096, lq=4, n_docs=500, n_tok=16000), 4),
 ])
 def test_loss_rejects(kw, status):
     assert _loss(**kw) == status
@@ -109,7 +111,7 @@ def _total(**kw):
     (dict(scale=float("nan")), 1), (dict(tau=0.0), 1), (dict(tau=-0.05), 1),
     (dict(tau=float("nan")), 1), (dict(tau=float("inf")), 1), (dict(tau=1e-40), 1),
     (dict(nq=1024, lq=32), 4), (dict(dd=FAKE_ODD), 1), (dict(lq=65), 4), (dict(dim=12), 4),
-    (dict(ws_bytes=100), 5),
+    (dict(ws_bytes=100), 5), (dict(nq=512, lq=32, n_docs=500, n_tok=16000), 4),
 ])
 def test_total_loss_rejects(kw, status):
     assert _total(**kw) == status

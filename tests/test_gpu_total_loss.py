@@ -2,7 +2,7 @@
 against the fp64 oracle (oracle.coltrast_total_loss), through the C ABI.
 
 Tolerances: the three losses within relative 2e-3 (the bar for scores and loss); gradients
-within relative L2 error 2e-3 per tensor; where the L_LI half of a document row is zero (no
+within relative L2 error 2e-3 per tensor and per row (tests/grad_check.py); where the L_LI half of a document row is zero (no
 query token selects the row) the row is half of L_C's gradient alone, checked element by
 element within 2e-3 of the row's largest entry.
 """
@@ -16,6 +16,7 @@ import torch
 import oracle
 import paper_2505_04846_amd as hpr
 import synth
+from grad_check import check_rows, near_tie_allowance
 
 pytestmark = pytest.mark.gpu
 
@@ -62,6 +63,10 @@ def _parity(Q, D, off, pos, scale, tau):
     # dot products may select another token in fp32) carry L_C's part alone: check them entry
     # by entry
     li = oracle.coltrast_li_loss(Qo, Do, off.numpy(), pos.numpy(), scale)
+    # every row on its own (the L_LI half's dL/dS is G / 2)
+    aq, ad, _ = near_tie_allowance(Qo, Do, off.numpy(), 0.5 * li["G"])
+    check_rows(dq, o["dQ"], aq, "dQ rows")
+    check_rows(dd, o["dD"], ad, "dD rows")
     li_gpu = hpr.coltrast_loss_fwd_bwd(*_to_dev(Q, D, off, pos), scale)["dd"].cpu().numpy()
     c = oracle.contrastive_loss(Qo, Do, off.numpy(), pos.numpy(), tau)
     free = ~np.any(li["dD"] != 0, axis=1) & ~np.any(li_gpu != 0, axis=1)
