@@ -17,7 +17,8 @@ Steps, in order:
   1. P_q = mean_i Q[q, i, :];  P_d = mean_{j in d} D[j, :];
   2. U = P / |P| (rows);  C[q, d] = <U_q, U_d> / tau;
   3. L_C = (1/B) sum_q (logsumexp_d C[q, d] - C[q, pos[q]]);
-  4. dL_C/dC = (1/B) (softmax_d C[q, :] - onehot(pos[q]));
+  4. dL_C/dC = (1/B) (softmax_d C[q, :] - onehot(pos[q])), the positive's entry taken as minus the sum
+     of the other probabilities (the same number, without cancellation in float64);
   5. dL_C/dU_q = (1/tau) sum_d dC[q, d] U_d;  dL_C/dU_d = (1/tau) sum_q dC[q, d] U_q;
   6. dL_C/dP = (dU - U <U, dU>) / |P|   (the normalisation's Jacobian);
   7. dL_C/dQ[q, i] = dL_C/dP_q / lq;  dL_C/dD[j] = dL_C/dP_d / L_d for every token j of d.
@@ -63,9 +64,11 @@ def contrastive_loss(Q, D, offsets, pos, tau):
     rows = np.arange(nq)
     loss = (lse - C[rows, pos]).sum() / nq
 
-    # 4
+    # 4 (the positive's softmax - 1 as minus the other probabilities: the same number, without
+    # the cancellation of 1 - p in float64 when p is within ~1e-13 of 1)
     dC = np.exp(C - lse[:, None])
-    dC[rows, pos] -= 1.0
+    for q in range(nq):
+        dC[q, pos[q]] = -np.delete(dC[q], pos[q]).sum()
     dC /= nq
 
     # 5-6

@@ -14,7 +14,11 @@ Steps, in order:
   2. logits l = s * S;
   3. LSE_q = M_q + log sum_d exp(l[q, d] - M_q) with M_q = max_d l[q, d];
   4. loss = (1/B) sum_q (LSE_q - l[q, pos[q]]);
-  5. G[q, d] = dloss/dS[q, d] = (s/B) * (exp(l[q, d] - LSE_q) - [d == pos[q]]);
+  5. G[q, d] = dloss/dS[q, d] = (s/B) * (exp(l[q, d] - LSE_q) - [d == pos[q]]); for the positive,
+     exp(l - LSE) - 1 is evaluated as minus the sum of the other documents' probabilities (the
+     probabilities sum to one, so this is the same number): when the positive's probability is
+     within ~1e-13 of 1, as at a logit scale of 50, 1 - p rounds to 0 in float64 while the sum of
+     the others keeps every digit;
   6. dQ[q, i, :] = sum_d G[q, d] * D[off[d] + A[q, i, d], :]           (chain rule through the max);
   7. dD[j, :]    = sum over (q, i, d) with off[d] + A[q, i, d] == j of G[q, d] * Q[q, i, :].
 """
@@ -50,7 +54,8 @@ def coltrast_li_loss(Q, D, offsets, pos, logit_scale):
 
     # 5
     G = np.exp(logits - lse[:, None])
-    G[rows, pos] -= 1.0
+    for q in range(nq):
+        G[q, pos[q]] = -np.delete(G[q], pos[q]).sum()   # p_pos - 1 = -(sum of the others)
     G *= s / nq
 
     # 6: for each (q, d), every query token i picks up G[q, d] times its maximising doc token
