@@ -105,6 +105,25 @@ hpr_status maxsim_score(const uint16_t* q, int32_t nq, int32_t lq,
                         void* ws, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------------------------
+ * maxsim_score_noalloc -- maxsim_score for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid allocation): no workspace
+ * argument, and no hipMalloc, hipFree or allocating library routine on any path.
+ *
+ * Same arguments, results (bit for bit) and kernels as maxsim_score, except that the scratch
+ * (the document-range table, at most 65,536 ranges) lives in a static device array of
+ * 65,537 int64 (512 KiB + 8 bytes) that each GPU the library runs on holds until the process
+ * ends.  Every call on a GPU shares that GPU's array, so calls that overlap on one GPU (on
+ * different streams or host threads) race and give unspecified scores; calls in order on one
+ * stream are safe.  The array's address is looked up on the first call on each device.
+ *
+ *   Returns HPR_ERR_UNSUPPORTED_SHAPE if a shape would need more ranges than the array holds
+ *   (the range count is capped at 65,536, so this does not happen for any accepted shape).
+ * ------------------------------------------------------------------------------------------- */
+hpr_status maxsim_score_noalloc(const uint16_t* q, int32_t nq, int32_t lq,
+                                const uint16_t* d_tok, const int64_t* d_off, int64_t n_docs,
+                                int64_t n_tok, int32_t dim, float* scores, void* stream);
+
+/* ---------------------------------------------------------------------------------------------
  * maxsim_topk -- exact top-k documents of each query under MaxSim.
  *
  * Retrieval returns the IDs of a query's nearest neighbours in the chunk store (Sec. 2.3);

@@ -5,6 +5,7 @@ torch provides device memory (outputs and workspaces) and the current stream.  T
 fallback: if the library is not built, or a call fails, an exception is raised.
 
     maxsim_score(Q, D, off)                       -> scores fp32 [nq, n_docs]
+    maxsim_score_noalloc(Q, D, off)               -> the same, with no device allocation
     maxsim_topk(Q, D, off, k)                     -> (scores fp32 [nq, k], idx int64 [nq, k])
     coltrast_loss_fwd_bwd(Q, D, off, pos, scale)  -> dict(loss, dq, dd, scores)
     coltrast_loss(Q, D, off, pos, scale)          -> loss with autograd to Q and D
@@ -57,6 +58,7 @@ _F32 = ctypes.c_float
 
 _SIGNATURES = {
     "maxsim_score": (_I32, [_P, _I32, _I32, _P, _P, _I64, _I64, _I32, _P, _P, _SZ, _P]),
+    "maxsim_score_noalloc": (_I32, [_P, _I32, _I32, _P, _P, _I64, _I64, _I32, _P, _P]),
     "maxsim_topk": (_I32, [_P, _I32, _I32, _P, _P, _I64, _I64, _I32, _I32, _P, _P, _P, _SZ, _P]),
     "coltrast_loss_fwd_bwd": (_I32, [_P, _I32, _I32, _P, _P, _I64, _I64, _I32, _P, _F32,
                                      _P, _P, _P, _P, _P, _SZ, _P]),
@@ -153,6 +155,21 @@ def maxsim_score(Q, D, off, ws=None):
     with torch.cuda.device(dev):
         _check(L.maxsim_score(_ptr(Q), nq, lq, _ptr(D), _ptr(off), n_docs, n_tok, dim,
                               _ptr(scores), _ptr(ws), ws.numel(), _stream(dev)))
+    return scores
+
+
+def maxsim_score_noalloc(Q, D, off, out=None):
+    """maxsim_score through the entry point that allocates no device memory (its scratch is a
+    static array of the library); `out` may be a preallocated fp32 [nq, n_docs] tensor."""
+    dev, nq, lq, dim, n_docs, n_tok = _maxsim_inputs(Q, D, off)
+    scores = out if out is not None else torch.empty((nq, n_docs), dtype=torch.float32,
+                                                     device=dev)
+    _need(scores, "out", torch.float32, 2, dev)
+    if tuple(scores.shape) != (nq, n_docs):
+        raise ValueError(f"out must be [{nq}, {n_docs}]")
+    with torch.cuda.device(dev):
+        _check(lib().maxsim_score_noalloc(_ptr(Q), nq, lq, _ptr(D), _ptr(off), n_docs, n_tok, dim,
+                                          _ptr(scores), _stream(dev)))
     return scores
 
 

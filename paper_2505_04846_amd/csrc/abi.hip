@@ -60,6 +60,35 @@ hpr_status current_cu_count(int* n_cu) {
   return HPR_OK;
 }
 
+// Scratch of maxsim_score_noalloc: the score kernel's document-range table (at most kMaxRanges
+// ranges, kMaxRanges + 1 int64 entries: 512 KiB + 8 bytes), one copy per GPU, held until the
+// process ends.  Host code never uses `scratch` itself as an address: each device's address is
+// looked up once (hipGetSymbolAddress, with that device current) and kept in g_scratch_ptr.
+constexpr size_t kScratchEntries = (size_t)kMaxRanges + 1;
+static __device__ __align__(256) int64_t scratch[kScratchEntries];
+std::mutex g_scratch_mu;
+int64_t* g_scratch_ptr[kMaxDevices];
+
+// Device address of the current device's `scratch` (looked up on the first call per device).
+hpr_status scratch_address(int64_t** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(HPR_ERR_UNSUPPORTED_SHAPE, "device %d beyond the %d this build tracks", dev,
+                kMaxDevices);
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(HPR_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = static_cast<int64_t*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return HPR_OK;
+}
+
 // Optional per-kernel timing: when enabled, every launch made through `timed` is bracketed by
 // two HIP events recorded on the launch stream; hpr_kernel_timing_read sums their durations.
 std::atomic<int> g_timing_on{0};
@@ -303,6 +332,34 @@ hpr_status maxsim_score(const uint16_t* q, int32_t nq, int32_t lq, const uint16_
   int64_t* part = c.take<int64_t>(part_bytes(n_docs));
   return run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, scores, nullptr, nullptr, 0,
                     part, static_cast<hipStream_t>(stream));
+}
+
+hpr_status maxsim_score_noalloc(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d_tok,
+                                const int64_t* d_off, int64_t n_docs, int64_t n_tok, int32_t dim,
+                                float* scores, void* stream) {
+  hpr_status st = check_maxsim_args(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim);
+  if (st == HPR_OK) st = check_lq(lq, dim, false);
+  if (st != HPR_OK) return st;
+  if (!scores) return fail(HPR_ERR_INVALID_ARG, "scores must be non-NULL");
+  int n_cu = 0;
+  st = current_cu_count(&n_cu);
+  if (st != HPR_OK) return st;
+  MaxsimPlan plan;
+  if (!maxsim_plan(nq, lq, n_docs, n_tok, dim, false, n_cu, &plan))
+    return fail(HPR_ERR_UNSUPPORTED_SHAPE, "no MaxSim plan for this shape");
+  if ((size_t)plan.n_ranges + 1 > kScratchEntries)
+    return fail(HPR_ERR_UNSUPPORTED_SHAPE, "%d document ranges exceed the %zu-entry scratch",
+                plan.n_ranges, kScratchEntries - 1);
+  int64_t* part = nullptr;
+  st = scratch_address(&part);
+  if (st != HPR_OK) return st;
+  // The same two launches as maxsim_score (partition, then scores), without the timing events.
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = launch_partition(d_off, n_docs, n_tok, plan.n_ranges, part, nullptr, 0, s);
+  if (e != hipSuccess) return hip_fail(e, "partition launch");
+  e = launch_maxsim(plan, q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, part, scores, nullptr,
+                    nullptr, 0, s);
+  return e == hipSuccess ? HPR_OK : hip_fail(e, "maxsim launch");
 }
 
 hpr_status maxsim_topk(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d_tok,

@@ -63,6 +63,19 @@ def test_maxsim_score_rejects(kw, status):
     assert hpr.lib().hpr_last_error()  # a message is set
 
 
+@pytest.mark.parametrize("kw,status", [
+    (dict(q=NULL), 1), (dict(d=NULL), 1), (dict(off=NULL), 1), (dict(scores=NULL), 1),
+    (dict(nq=0), 1), (dict(n_tok=3), 1), (dict(dim=12), 4), (dict(lq=129), 4),
+    (dict(q=FAKE_ODD), 1),
+])
+def test_maxsim_score_noalloc_rejects(kw, status):
+    a = dict(q=FAKE, nq=2, lq=32, d=FAKE, off=FAKE, n_docs=4, n_tok=64, dim=128, scores=FAKE)
+    a.update(kw)
+    assert hpr.lib().maxsim_score_noalloc(a["q"], a["nq"], a["lq"], a["d"], a["off"], a["n_docs"],
+                                          a["n_tok"], a["dim"], a["scores"], NULL) == status
+    assert hpr.lib().hpr_last_error()
+
+
 def _topk(k, n_docs=10, ws_bytes=BIG):
     return hpr.lib().maxsim_topk(FAKE, 2, 8, FAKE, FAKE, n_docs, 100, 64, k, FAKE, FAKE, FAKE,
                                  ws_bytes, NULL)
