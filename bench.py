@@ -38,8 +38,8 @@ PEAK_HBM_GBS = 8000.0
 COPY_CALIBRATION_BYTES = 256 << 20  # bytes read (and written) by each calibration copy
 CPU_SAMPLE_SECONDS = 10.0  # the oracle sample is repeated for at least this long
 KERNELS = ("partition", "maxsim", "maxsim_argmax", "topk", "infonce", "pool", "contrastive",
-           "grad_q", "grad_d", "dense_sample", "dense_scan", "dense_merge", "semantic_chunk",
-           "retrieval_metrics")
+           "grad_q", "grad_d", "dense_sample", "dense_scan", "dense_merge", "dense_fallback",
+           "semantic_chunk", "retrieval_metrics")
 
 
 def parse():
@@ -296,7 +296,7 @@ def build_workload(name, dev, scale, tau, nq_sub=None):
         return dict(step=step, pairs=nq, kernel="dense_scan", flops=flops, bytes=sbytes, after=after,
                     metric="top-k queries/sec + % fp16 MFMA peak",
                     cpu_sample=cpu_sample, config=cfg, dtype="fp16", unit="queries/s",
-                    sha=source_sha("dense.hip", "common.h"), graph=False)
+                    sha=source_sha("dense.hip", "common.h"))
 
     if name == "semantic_chunk":
         w = synth.sentence_stream(seed=0, device=dev)

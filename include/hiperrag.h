@@ -63,7 +63,7 @@ typedef int32_t hpr_status;
 #define HPR_ERR_EMPTY_DOC 3           /* hpr_csr_validate: a document with no token            */
 #define HPR_ERR_UNSUPPORTED_SHAPE 4   /* valid, but outside the limits this build supports     */
 #define HPR_ERR_WORKSPACE_TOO_SMALL 5 /* ws_bytes below the *_workspace_size() value            */
-#define HPR_ERR_CAPACITY 6            /* dense_ip_topk: candidate lists kept overflowing (see it) */
+#define HPR_ERR_CAPACITY 6            /* reserved: no entry point of this version returns it    */
 #define HPR_ERR_HIP 7                 /* a HIP runtime call or kernel launch failed             */
 
 #define HPR_ABI_VERSION 1
@@ -213,9 +213,16 @@ hpr_status coltrast_total_loss_fwd_bwd(const uint16_t* q, int32_t nq, int32_t lq
  * each pooled chunk embedding and returns the nearest neighbours' IDs (Sec. 3.2.1 "Similarity
  * metric"; Sec. 4.2; Sec. 2.3).  For L2-normalised rows the cosine is the inner product:
  *     s[q,n] = <Q[q,:], X[n,:]>  (fp16 x fp16 products, fp32 accumulation)
- * Results are sorted by score descending, equal scores by lower row index first.
+ * Results are sorted by score descending, equal scores by lower row index first.  Exact for any
+ * input (no approximate index): the score matrix is never stored; rows past an exactly scored
+ * sample are kept only when they beat the sample's k-th key, and a query whose candidate list
+ * overflows the workspace's capacity (adversarial stores: thousands of rows above that key) is
+ * finished on the device by a radix select over rescans of the store.  Like every call it is
+ * asynchronous (no host synchronisation, no status decided on the device), so it can be
+ * captured in a HIP graph; it never returns HPR_ERR_CAPACITY.
  *
  *   q   fp16 [nq, dim]; x fp16 [n, dim]; out_scores fp32 [nq, k]; out_idx int64 [nq, k].
+ *   ws  workspace of dense_ip_topk_workspace_size(...) bytes.
  * ------------------------------------------------------------------------------------------- */
 hpr_status dense_ip_topk(const uint16_t* q, int32_t nq, const uint16_t* x, int64_t n,
                          int32_t dim, int32_t k, float* out_scores, int64_t* out_idx,
@@ -312,7 +319,8 @@ hpr_status hpr_read_calibration(const void* buf, int64_t bytes, uint32_t* sink, 
  * bracketed by two HIP events recorded on its launch stream.  hpr_kernel_timing_read
  * synchronises on the events recorded for kernel `name` ("partition", "maxsim",
  * "maxsim_argmax", "topk", "infonce", "pool", "contrastive", "grad_q", "grad_d",
- * "dense_sample", "dense_scan", "dense_merge", "semantic_chunk", "retrieval_metrics",
+ * "dense_sample", "dense_scan", "dense_merge", "dense_fallback", "semantic_chunk",
+ * "retrieval_metrics",
  * "mfma_calibration", "read_calibration"), returns
  * the sum of their durations in milliseconds and the launch count, and forgets them. */
 hpr_status hpr_kernel_timing(int32_t enable);

@@ -508,8 +508,10 @@ size_t dense_ip_topk_workspace_size(int32_t nq, int64_t n, int32_t dim, int32_t 
        align_up((size_t)nq * sizeof(int32_t));
   b += align_up((size_t)nq * (size_t)p.cap * sizeof(float)) +
        align_up((size_t)nq * (size_t)p.cap * sizeof(uint32_t));
-  b += 2 * align_up(sizeof(int32_t)) + 2 * align_up((size_t)nq * sizeof(int32_t));
-  b += align_up((size_t)nq * (size_t)dim * sizeof(uint16_t));
+  b += align_up(sizeof(int32_t)) + align_up((size_t)nq * sizeof(int32_t));   // queue
+  b += align_up((size_t)nq * (size_t)dim * sizeof(uint16_t));                   // queued rows
+  b += align_up((size_t)nq * 256 * sizeof(uint32_t)) +                          // radix select
+       align_up((size_t)nq * sizeof(unsigned long long)) + align_up((size_t)nq * sizeof(uint32_t));
   return b;
 }
 
@@ -532,14 +534,24 @@ hpr_status dense_ip_topk(const uint16_t* q, int32_t nq, const uint16_t* x, int64
   const size_t need = dense_ip_topk_workspace_size(nq, n, dim, k);
   if (ws_bytes < need)
     return fail(HPR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu < %zu bytes", ws_bytes, need);
+  int n_cu = 0;
+  hpr_status st = current_cu_count(&n_cu);
+  if (st != HPR_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const DensePlan p = dense_plan(n, k);
   Carver c(ws);
   float* sample = c.take<float>((size_t)nq * (size_t)p.S * sizeof(float));
-  hipError_t e = timed("dense_sample", s, [&] {
-    return launch_dense_gemm(false, q, nq, nullptr, x, 0, p.S, dim, sample, p.S, nullptr, nullptr,
-                             nullptr, nullptr, nullptr, 0, s);
-  });
+  DenseGemm g = {};
+  g.mode = 0;
+  g.q = q;
+  g.nqa = nq;
+  g.x = x;
+  g.r0 = 0;
+  g.r1 = p.S;
+  g.dim = dim;
+  g.scores = sample;
+  g.ld = p.S;
+  hipError_t e = timed("dense_sample", s, [&] { return launch_dense_gemm(g, n_cu, s); });
   if (e != hipSuccess) return hip_fail(e, "dense sample launch");
   if (p.S == n) {  // the sample is the whole store
     e = timed("topk", s, [&] {
@@ -554,54 +566,65 @@ hpr_status dense_ip_topk(const uint16_t* q, int32_t nq, const uint16_t* x, int64
   int32_t* count = c.take<int32_t>((size_t)nq * sizeof(int32_t));
   float* cand_s = c.take<float>((size_t)nq * (size_t)p.cap * sizeof(float));
   uint32_t* cand_i = c.take<uint32_t>((size_t)nq * (size_t)p.cap * sizeof(uint32_t));
-  int32_t* ctrl[2];
-  int32_t* qlist[2];
-  ctrl[0] = c.take<int32_t>(sizeof(int32_t));
-  ctrl[1] = c.take<int32_t>(sizeof(int32_t));
-  qlist[0] = c.take<int32_t>((size_t)nq * sizeof(int32_t));
-  qlist[1] = c.take<int32_t>((size_t)nq * sizeof(int32_t));
+  int32_t* n_queued = c.take<int32_t>(sizeof(int32_t));
+  int32_t* qlist = c.take<int32_t>((size_t)nq * sizeof(int32_t));
   uint16_t* qc = c.take<uint16_t>((size_t)nq * dim * sizeof(uint16_t));
+  uint32_t* hist = c.take<uint32_t>((size_t)nq * 256 * sizeof(uint32_t));
+  unsigned long long* prefix = c.take<unsigned long long>((size_t)nq * sizeof(unsigned long long));
+  uint32_t* remaining = c.take<uint32_t>((size_t)nq * sizeof(uint32_t));
 
   e = timed("topk", s, [&] { return launch_topk_rows(sample, nq, p.S, p.S, k, ss, si, s); });
   if (e != hipSuccess) return hip_fail(e, "top-k launch");
-  e = launch_dense_init(ss, nq, k, theta, tie, count, s);
+  e = launch_dense_init(ss, nq, k, theta, tie, count, n_queued, s);
   if (e != hipSuccess) return hip_fail(e, "dense init launch");
-  e = timed("dense_scan", s, [&] {
-    return launch_dense_gemm(true, q, nq, nullptr, x, p.S, n, dim, nullptr, 0, theta, tie, count,
-                             cand_s, cand_i, p.cap, s);
-  });
+  g.mode = 1;
+  g.r0 = p.S;
+  g.r1 = n;
+  g.scores = nullptr;
+  g.ld = 0;
+  g.theta = theta;
+  g.tie = tie;
+  g.count = count;
+  g.cand_s = cand_s;
+  g.cand_i = cand_i;
+  g.cap = p.cap;
+  e = timed("dense_scan", s, [&] { return launch_dense_gemm(g, n_cu, s); });
   if (e != hipSuccess) return hip_fail(e, "dense scan launch");
   e = timed("dense_merge", s, [&] {
-    return launch_dense_merge(ss, si, nq, k, count, cand_s, cand_i, p.cap, nullptr, out_scores, out_idx, theta, tie, ctrl[0], qlist[0], s);
+    return launch_dense_merge(ss, si, nq, k, count, cand_s, cand_i, p.cap, nullptr, nullptr,
+                              out_scores, out_idx, theta, tie, n_queued, qlist, prefix, remaining,
+                              s);
   });
   if (e != hipSuccess) return hip_fail(e, "dense merge launch");
-  // Overflowed candidate lists (none unless the sample bound is far from the k-th score) are
-  // rescanned with their raised bounds until every list fits.
-  int cur = 0;
-  for (int round = 0;; ++round) {
-    int32_t m = 0;
-    e = hipMemcpyAsync(&m, ctrl[cur], sizeof(m), hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
-    if (e != hipSuccess) return hip_fail(e, "dense overflow check");
-    if (m == 0) return HPR_OK;
-    if (round == kDenseMaxRepairs)
-      return fail(HPR_ERR_CAPACITY, "candidate lists of %d queries still overflow after %d rescans",
-                  m, kDenseMaxRepairs);
-    const int nxt = cur ^ 1;
-    e = launch_dense_repair_prep(q, dim, qlist[cur], m, qc, count, s);
+  // Exact fallback for the queued queries (their lists overflowed): every launch below reads
+  // the queue length on the device and does nothing when it is 0.  A radix select over the
+  // rescanned keys (8 bytes, most significant first) finds each queued query's k-th key;
+  // one more rescan collects the keys at or above it (at most k) and the merge rewrites the
+  // query's output.
+  e = launch_dense_fallback_prep(q, dim, qlist, n_queued, qc, hist, n_cu, s);
+  if (e != hipSuccess) return hip_fail(e, "dense fallback launch");
+  DenseGemm f = g;
+  f.q = qc;
+  f.qmap = qlist;
+  f.m_dev = n_queued;
+  f.hist = hist;
+  f.prefix = prefix;
+  for (int shift = 56; shift >= 0; shift -= 8) {
+    f.mode = 2;
+    f.shift = shift;
+    e = timed("dense_fallback", s, [&] { return launch_dense_gemm(f, n_cu, s); });
     if (e == hipSuccess)
-      e = timed("dense_scan", s, [&] {
-        return launch_dense_gemm(true, qc, m, qlist[cur], x, p.S, n, dim, nullptr, 0, theta, tie,
-                                 count, cand_s, cand_i, p.cap, s);
-      });
-    if (e == hipSuccess)
-      e = timed("dense_merge", s, [&] {
-        return launch_dense_merge(ss, si, m, k, count, cand_s, cand_i, p.cap, qlist[cur], out_scores,
-                                  out_idx, theta, tie, ctrl[nxt], qlist[nxt], s);
-      });
-    if (e != hipSuccess) return hip_fail(e, "dense repair launch");
-    cur = nxt;
+      e = launch_dense_radix(n_queued, qlist, nq, shift, ss, si, k, hist, prefix, remaining,
+                             theta, tie, count, s);
+    if (e != hipSuccess) return hip_fail(e, "dense fallback launch");
   }
+  f.mode = 1;
+  e = timed("dense_fallback", s, [&] { return launch_dense_gemm(f, n_cu, s); });
+  if (e == hipSuccess)
+    e = launch_dense_merge(ss, si, nq, k, count, cand_s, cand_i, p.cap, qlist, n_queued,
+                           out_scores, out_idx, theta, tie, nullptr, nullptr, nullptr, nullptr,
+                           s);
+  return e == hipSuccess ? HPR_OK : hip_fail(e, "dense fallback launch");
 }
 
 hpr_status hpr_csr_validate(const int64_t* d_off, int64_t n_docs, int64_t n_tok, void* ws,

@@ -11,9 +11,17 @@
 //      its query's candidate list only when its key beats the query's bound.  With a random
 //      sample the expected list length is about k (n - S) / S.
 //   3. Merge.  Per query, the exact top-k of (sample top-k) U (candidates) under a unique
-//      64-bit key (score key, ~row).  A list that overflowed its capacity is repaired: its
-//      bound is raised to the k-th key found so far (still a valid bound: k rows reach it) and
-//      rows [S, n) are rescanned for those queries only, until no list overflows.
+//      64-bit key (score key, ~row).  A query whose list overflowed its capacity is queued (its
+//      bound raised to the k-th key found so far, still a valid bound: k rows reach it).
+//   4. Exact fallback for the queued queries, decided on the device: the k-th largest key of
+//      {keys >= bound} by a radix select over the GEMM itself -- 8 rescans of rows [S, n), each
+//      counting one byte of the 64-bit keys into per-query 256-bin histograms (in LDS, then
+//      added to global memory), with the sample's entries counted by the select step -- then
+//      one rescan that collects the keys >= that k-th key (exactly k with the sample's: keys
+//      are unique, so the list cannot overflow) and a final merge.  These launches use
+//      persistent grids that read the number of queued queries from the device and exit at
+//      once when it is 0, so the call never synchronises with the host and is capturable in a
+//      HIP graph.
 //
 // GEMM tile: 256 queries x 256 rows per 8-wave workgroup (each wave 64 x 128 = 2 x 4 blocks of
 // v_mfma_f32_32x32x16_f16; 128 x 128 per wave at one wave per SIMD measured 20 % slower); K advances 32 halves per stage through a 4-deep LDS ring filled by
@@ -84,25 +92,31 @@ struct GemmArgs {
   float* cand_s;          // [nq, cap]
   uint32_t* cand_i;       // [nq, cap]
   int64_t cap;
+  // persistent launches: the number of queries (rows of q, entries of qmap) is *m_dev
+  const int32_t* m_dev;
+  // histogram mode: per local query, 256 bins of byte `shift / 8` of the keys >= the bound
+  // whose bits above that byte equal prefix[global query]
+  uint32_t* hist;                       // [m, 256]
+  const unsigned long long* prefix;     // [nq]
+  int shift;
 };
 
-template <typename G, bool FILTER>
-__global__ __launch_bounds__(G::kThreads, G::kMinWG) void dense_gemm_kernel(GemmArgs a) {
+enum GemmMode { kStore = 0, kFilter = 1, kHist = 2 };
+
+// One 256-row tile of X against query tile qt (queries [qt kTQ, qt kTQ + kTQ) of the nqa of
+// the launch).
+template <typename G, int MODE>
+__device__ __forceinline__ void gemm_tile(const GemmArgs& a, int nqa, int qt, int rt,
+                                          unsigned char* smem) {
   constexpr int kTQ = G::kTQ, kTR = G::kTR, kKC = G::kKC, kStages = G::kStages;
   constexpr int kWQ = G::kWQ, kBQ = G::kBQ, kBR = G::kBR;
   constexpr int kRowBytes = G::kRowBytes, kQTileBytes = G::kQTileBytes;
   constexpr int kStageBytes = G::kStageBytes, kLoadsPerWave = G::kLoadsPerWave;
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wq = wave % kWQ;  // (32 kBQ)-query slice of the tile
   const int wr = wave / kWQ;  // (32 kBR)-row slice of the tile
-
-  const int64_t total = (int64_t)a.n_qt * a.n_rt;
-  const int64_t lin = xcd_linear(blockIdx.x, total);
-  const int rt = (int)(lin / a.n_qt);
-  const int qt = (int)(lin - (int64_t)rt * a.n_qt);
   const int q_base = qt * kTQ;
   const int64_t row_base = a.r0 + (int64_t)rt * kTR;
 
@@ -113,7 +127,7 @@ __global__ __launch_bounds__(G::kThreads, G::kMinWG) void dense_gemm_kernel(Gemm
   // (row within the tile, clamped to the last valid row, and chunk).
   const char* q_tile = reinterpret_cast<const char*>(a.q + (int64_t)q_base * a.dim);
   const char* x_tile = reinterpret_cast<const char*>(a.x + row_base * a.dim);
-  const int64_t q_rows = (int64_t)(a.nqa - q_base), x_rows = a.r1 - row_base;
+  const int64_t q_rows = (int64_t)(nqa - q_base), x_rows = a.r1 - row_base;
   uint32_t voff[kLoadsPerWave];
   int src_c[kLoadsPerWave];
   bool is_x[kLoadsPerWave];
@@ -236,13 +250,53 @@ __global__ __launch_bounds__(G::kThreads, G::kMinWG) void dense_gemm_kernel(Gemm
 
   // ---- epilogue.  acc[i][j] register r: query q_base + 32 kBQ wq + 32 i + 8 (r / 4) +
   // 4 half + r % 4, row row_base + 32 kBR wr + 32 j + col.
+  if constexpr (MODE == kHist) {
+    // per-tile histograms in LDS (the ring is no longer read once every wave has passed the
+    // barrier), then the non-zero bins added to the launch's histograms
+    static_assert(kTQ * 256 * 4 <= G::kStages * kStageBytes, "histograms fit the LDS ring");
+    uint32_t* hl = reinterpret_cast<uint32_t*>(smem);
+    barrier();
+    for (int e = tid; e < kTQ * 256; e += G::kThreads) hl[e] = 0u;
+    barrier();
+    const unsigned long long pmask = a.shift >= 56 ? 0ull : (~0ull << (a.shift + 8));
+#pragma unroll
+    for (int i = 0; i < kBQ; ++i) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int qo = 32 * kBQ * wq + 32 * i + 8 * (r >> 2) + 4 * half + (r & 3);
+        const int ql = q_base + qo;
+        if (ql >= nqa) continue;
+        const int gq = a.qmap[ql];
+        const float th = a.theta[gq];
+        const int64_t tie = a.tie[gq];
+        const unsigned long long pre = a.prefix[gq];
+#pragma unroll
+        for (int j = 0; j < kBR; ++j) {
+          const int64_t row = row_base + 32 * kBR * wr + 32 * j + col;
+          const float v = acc[i][j][r];
+          if (row < a.r1 && (v > th || (v == th && row <= tie))) {
+            const unsigned long long key =
+                ((unsigned long long)score_key(v) << 32) | (unsigned long long)(uint32_t)~(uint32_t)row;
+            if (((key ^ pre) & pmask) == 0ull)
+              atomicAdd(&hl[qo * 256 + (int)((key >> a.shift) & 255ull)], 1u);
+          }
+        }
+      }
+    }
+    barrier();
+    for (int e = tid; e < kTQ * 256; e += G::kThreads) {
+      const uint32_t c = hl[e];
+      if (c != 0u && q_base + (e >> 8) < nqa) atomicAdd(&a.hist[(int64_t)(q_base + (e >> 8)) * 256 + (e & 255)], c);
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < kBQ; ++i) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int ql = q_base + 32 * kBQ * wq + 32 * i + 8 * (r >> 2) + 4 * half + (r & 3);
-      if (ql >= a.nqa) continue;
-      if (!FILTER) {
+      if (ql >= nqa) continue;
+      if (MODE == kStore) {
         float* dst = a.scores + (int64_t)ql * a.ld + (row_base - a.r0) + 32 * kBR * wr + col;
 #pragma unroll
         for (int j = 0; j < kBR; ++j) {
@@ -270,26 +324,129 @@ __global__ __launch_bounds__(G::kThreads, G::kMinWG) void dense_gemm_kernel(Gemm
   }
 }
 
+// One tile per workgroup (workgroups sharing a row tile on one XCD), or, when PERSIST, a grid
+// that walks the tiles of the *m_dev queries of the launch (none when it is 0).
+template <typename G, int MODE, bool PERSIST>
+__global__ __launch_bounds__(G::kThreads, G::kMinWG) void dense_gemm_kernel(GemmArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  if constexpr (PERSIST) {
+    const int nqa = __builtin_amdgcn_readfirstlane(*a.m_dev);
+    if (nqa <= 0) return;
+    const int n_qt = (nqa + G::kTQ - 1) / G::kTQ;
+    const int64_t total = (int64_t)n_qt * a.n_rt;
+    for (int64_t t = blockIdx.x; t < total; t += gridDim.x) {
+      __syncthreads();  // the previous tile's LDS reads are complete before the ring refills
+      const int rt = (int)(t / n_qt);
+      gemm_tile<G, MODE>(a, nqa, (int)(t - (int64_t)rt * n_qt), rt, smem);
+    }
+  } else {
+    const int64_t total = (int64_t)a.n_qt * a.n_rt;
+    const int64_t lin = xcd_linear(blockIdx.x, total);
+    const int rt = (int)(lin / a.n_qt);
+    gemm_tile<G, MODE>(a, a.nqa, (int)(lin - (int64_t)rt * a.n_qt), rt, smem);
+  }
+}
+
 // Bound of every query from its sample top-k: theta = k-th score, strict comparison; lists
-// emptied.
+// emptied; the queue of overflowing queries emptied.
 __global__ void dense_init_kernel(const float* ss, int nq, int k, float* theta, int64_t* tie,
-                                  int32_t* count) {
+                                  int32_t* count, int32_t* n_queued) {
   const int q = blockIdx.x * blockDim.x + threadIdx.x;
+  if (q == 0) *n_queued = 0;
   if (q >= nq) return;
   theta[q] = ss[(int64_t)q * k + k - 1];
   tie[q] = -1;
   count[q] = 0;
 }
 
-// Queries to rescan: their Q rows are gathered (qc) and their lists emptied.
-__global__ void dense_repair_prep_kernel(const uint16_t* q, int dim, const int32_t* qlist,
-                                         int m, uint16_t* qc, int32_t* count) {
+// Queued queries (*m_dev of them): their Q rows are gathered into qc and their histograms
+// zeroed.
+__global__ void dense_fallback_prep_kernel(const uint16_t* q, int dim, const int32_t* qlist,
+                                           const int32_t* m_dev, uint16_t* qc, uint32_t* hist) {
+  const int m = *m_dev;
   for (int i = blockIdx.x; i < m; i += gridDim.x) {
     const int gq = qlist[i];
     const u32x4* s = reinterpret_cast<const u32x4*>(q + (int64_t)gq * dim);
     u32x4* d = reinterpret_cast<u32x4*>(qc + (int64_t)i * dim);
     for (int c = threadIdx.x; c < dim / 8; c += blockDim.x) d[c] = s[c];
-    if (threadIdx.x == 0) count[gq] = 0;
+    for (int c = threadIdx.x; c < 256; c += blockDim.x) hist[(int64_t)i * 256 + c] = 0u;
+  }
+}
+
+// One radix step of the exact fallback for queued query i (one workgroup each; none past
+// *m_dev): the query's scan histogram (hist[i], then zeroed for the next pass) plus its sample
+// top-k entries with key >= the bound and the same prefix give the byte of the k-th key at
+// `shift`; after the last byte (shift 0) the bound becomes that key, inclusive, and the list is
+// emptied for the collecting rescan.
+__global__ __launch_bounds__(256) void dense_radix_kernel(
+    const int32_t* m_dev, const int32_t* qlist, int shift, const float* ss, const int64_t* si,
+    int k, uint32_t* hist, unsigned long long* prefix, uint32_t* remaining, float* theta,
+    int64_t* tie, int32_t* count) {
+  __shared__ uint32_t h[256];
+  __shared__ uint32_t sh_bin, sh_above;
+  const int i = blockIdx.x;
+  if (i >= *m_dev) return;  // uniform
+  const int q = qlist[i];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const unsigned long long pmask = shift >= 56 ? 0ull : (~0ull << (shift + 8));
+  const unsigned long long pre = prefix[q];
+  const float th = theta[q];
+  const int64_t tb = tie[q];
+  h[tid] = hist[(int64_t)i * 256 + tid];
+  hist[(int64_t)i * 256 + tid] = 0u;
+  if (tid == 0) {
+    sh_bin = 0u;
+    sh_above = 0u;
+  }
+  __syncthreads();
+  for (int e = tid; e < k; e += 256) {
+    const float v = ss[(int64_t)q * k + e];
+    const int64_t row = si[(int64_t)q * k + e];
+    if (v > th || (v == th && row <= tb)) {
+      const unsigned long long key =
+          ((unsigned long long)score_key(v) << 32) | (unsigned long long)(uint32_t)~(uint32_t)row;
+      if (((key ^ pre) & pmask) == 0ull) atomicAdd(&h[(int)((key >> shift) & 255ull)], 1u);
+    }
+  }
+  __syncthreads();
+  const uint32_t rem = remaining[q];
+  if (wave == 0) {  // the bin holding the rem-th largest key, counting from bin 255 down
+    uint32_t c[4], tot = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      c[j] = h[255 - 4 * lane - j];
+      tot += c[j];
+    }
+    uint32_t incl = tot;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = __shfl_up(incl, o);
+      if (lane >= o) incl += y;
+    }
+    const uint32_t excl = incl - tot;
+    if (excl < rem && rem <= incl) {
+      uint32_t accu = excl;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (accu + c[j] >= rem) {
+          sh_bin = 255u - 4u * lane - j;
+          sh_above = accu;
+          break;
+        }
+        accu += c[j];
+      }
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const unsigned long long np = pre | ((unsigned long long)sh_bin << shift);
+    prefix[q] = np;
+    remaining[q] = rem - sh_above;
+    if (shift == 0) {  // np is the k-th largest key: collect every key >= it
+      theta[q] = key_score((uint32_t)(np >> 32));
+      tie[q] = (int64_t)(uint32_t)~(uint32_t)np;
+      count[q] = 0;
+    }
   }
 }
 
@@ -298,16 +455,19 @@ constexpr int kMergeMaxK = 1024;
 
 // Exact top-k of (sample top-k of query q) U (its candidates) under the unique key
 // (score key << 32) | ~row: 8 radix passes of 8 bits find the k-th key K, the elements with key
-// >= K are gathered (exactly k: keys are unique) and bitonic-sorted.  A query whose list
-// overflowed gets its bound raised to K and is queued for a rescan (*ctrl_out counts them,
-// qlist_out lists them); its output is rewritten after the rescan.
+// >= K are gathered (exactly k: keys are unique) and bitonic-sorted.  With a queue
+// (n_queued != nullptr), a query whose list overflowed gets its bound raised to K, its radix
+// state reset (prefix 0, k keys to find) and is appended to qlist_out; its output is rewritten
+// by the fallback.  With m_dev, block b merges queued query qsel[b] when b < *m_dev.
 __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(
     const float* ss, const int64_t* si, int k, const int32_t* count, const float* cand_s,
-    const uint32_t* cand_i, int64_t cap, const int32_t* qsel, float* out_s, int64_t* out_i,
-    float* theta, int64_t* tie, int32_t* ctrl_out, int32_t* qlist_out) {
+    const uint32_t* cand_i, int64_t cap, const int32_t* qsel, const int32_t* m_dev,
+    float* out_s, int64_t* out_i, float* theta, int64_t* tie, int32_t* n_queued,
+    int32_t* qlist_out, unsigned long long* q_prefix, uint32_t* q_remaining) {
   __shared__ uint32_t hist[256];
   __shared__ unsigned long long sk[kMergeMaxK];
   __shared__ uint32_t sh_bin, sh_above, sh_n;
+  if (m_dev && (int)blockIdx.x >= *m_dev) return;  // uniform
   const int q = qsel ? qsel[blockIdx.x] : (int)blockIdx.x;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -411,95 +571,120 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(
     out_s[(int64_t)q * k + p] = key_score((uint32_t)(sk[p] >> 32));
     out_i[(int64_t)q * k + p] = (int64_t)(uint32_t)~(uint32_t)sk[p];
   }
-  if (cnt > cap && tid == 0) {
+  if (n_queued && cnt > cap && tid == 0) {
     theta[q] = key_score((uint32_t)(K >> 32));
     tie[q] = (int64_t)(uint32_t)~(uint32_t)K;
-    const int slot = atomicAdd(&ctrl_out[0], 1);
+    q_prefix[q] = 0ull;
+    q_remaining[q] = (uint32_t)k;
+    const int slot = atomicAdd(n_queued, 1);
     qlist_out[slot] = q;
   }
 }
-
-__global__ void dense_zero_ctrl_kernel(int32_t* ctrl) { ctrl[0] = 0; }
 
 }  // namespace
 
 namespace {
 
-template <typename G>
-hipError_t launch_gemm_t(bool filter, GemmArgs a, int64_t n_rt, hipStream_t stream) {
+template <typename G, int MODE, bool PERSIST>
+hipError_t launch_gemm_t(const GemmArgs& a, unsigned blocks, hipStream_t stream) {
+  const int lds = G::kStages * G::kStageBytes;
+  const void* fn = (const void*)dense_gemm_kernel<G, MODE, PERSIST>;
+  const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((dense_gemm_kernel<G, MODE, PERSIST>), dim3(blocks), dim3(G::kThreads), lds,
+                     stream, a);
+  return hipGetLastError();
+}
+
+template <typename G, int MODE>
+hipError_t launch_gemm_grid(GemmArgs a, int64_t n_rt, hipStream_t stream) {
   a.n_qt = (a.nqa + G::kTQ - 1) / G::kTQ;
   if (n_rt < 1 || n_rt > 0x7fffffffLL || (int64_t)a.n_qt * n_rt > 0xffffffffLL)
     return hipErrorInvalidValue;
   a.n_rt = (int)n_rt;
-  const int lds = G::kStages * G::kStageBytes;
-  const unsigned blocks = (unsigned)((int64_t)a.n_qt * n_rt);
-  const void* fn = filter ? (const void*)dense_gemm_kernel<G, true>
-                          : (const void*)dense_gemm_kernel<G, false>;
-  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-  if (e != hipSuccess) return e;
-  if (filter)
-    hipLaunchKernelGGL((dense_gemm_kernel<G, true>), dim3(blocks), dim3(G::kThreads), lds, stream,
-                       a);
-  else
-    hipLaunchKernelGGL((dense_gemm_kernel<G, false>), dim3(blocks), dim3(G::kThreads), lds,
-                       stream, a);
-  return hipGetLastError();
+  return launch_gemm_t<G, MODE, false>(a, (unsigned)((int64_t)a.n_qt * n_rt), stream);
 }
 
 }  // namespace
 
-hipError_t launch_dense_gemm(bool filter, const uint16_t* q, int nqa, const int32_t* qmap,
-                             const uint16_t* x, int64_t r0, int64_t r1, int dim, float* scores,
-                             int64_t ld, const float* theta, const int64_t* tie, int32_t* count,
-                             float* cand_s, uint32_t* cand_i, int64_t cap, hipStream_t stream) {
-  if (nqa < 1) return hipErrorInvalidValue;
-  GemmArgs a;
-  a.q = q;
-  a.x = x;
-  a.qmap = qmap;
-  a.nqa = nqa;
-  a.dim = dim;
-  a.r0 = r0;
-  a.r1 = r1;
-  a.scores = scores;
-  a.ld = ld;
-  a.theta = theta;
-  a.tie = tie;
-  a.count = count;
-  a.cand_s = cand_s;
-  a.cand_i = cand_i;
-  a.cap = cap;
-  const int64_t n_rt = (r1 - r0 + 255) / 256;
-  return nqa <= GeomNarrow::kTQ ? launch_gemm_t<GeomNarrow>(filter, a, n_rt, stream)
-                                : launch_gemm_t<GeomWide>(filter, a, n_rt, stream);
+hipError_t launch_dense_gemm(const DenseGemm& g, int n_cu, hipStream_t stream) {
+  if (g.nqa < 1 || g.r1 <= g.r0) return hipErrorInvalidValue;
+  GemmArgs a = {};
+  a.q = g.q;
+  a.x = g.x;
+  a.qmap = g.qmap;
+  a.nqa = g.nqa;
+  a.dim = g.dim;
+  a.r0 = g.r0;
+  a.r1 = g.r1;
+  a.scores = g.scores;
+  a.ld = g.ld;
+  a.theta = g.theta;
+  a.tie = g.tie;
+  a.count = g.count;
+  a.cand_s = g.cand_s;
+  a.cand_i = g.cand_i;
+  a.cap = g.cap;
+  a.m_dev = g.m_dev;
+  a.hist = g.hist;
+  a.prefix = g.prefix;
+  a.shift = g.shift;
+  const int64_t n_rt = (g.r1 - g.r0 + 255) / 256;
+  if (g.m_dev) {  // persistent narrow-tile grid over the *m_dev queued queries
+    if (n_rt > 0x7fffffffLL || !g.qmap) return hipErrorInvalidValue;
+    a.n_rt = (int)n_rt;
+    const unsigned blocks = (unsigned)((n_cu > 0 ? n_cu : 256) * GeomNarrow::kMinWG);
+    if (g.mode == kHist) return launch_gemm_t<GeomNarrow, kHist, true>(a, blocks, stream);
+    if (g.mode == kFilter) return launch_gemm_t<GeomNarrow, kFilter, true>(a, blocks, stream);
+    return hipErrorInvalidValue;
+  }
+  const bool narrow = g.nqa <= GeomNarrow::kTQ;
+  switch (g.mode) {
+    case kStore:
+      return narrow ? launch_gemm_grid<GeomNarrow, kStore>(a, n_rt, stream)
+                    : launch_gemm_grid<GeomWide, kStore>(a, n_rt, stream);
+    case kFilter:
+      return narrow ? launch_gemm_grid<GeomNarrow, kFilter>(a, n_rt, stream)
+                    : launch_gemm_grid<GeomWide, kFilter>(a, n_rt, stream);
+    default:
+      return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_dense_init(const float* ss, int nq, int k, float* theta, int64_t* tie,
-                             int32_t* count, hipStream_t stream) {
+                             int32_t* count, int32_t* n_queued, hipStream_t stream) {
   hipLaunchKernelGGL(dense_init_kernel, dim3((nq + 255) / 256), dim3(256), 0, stream, ss, nq, k,
-                     theta, tie, count);
+                     theta, tie, count, n_queued);
   return hipGetLastError();
 }
 
 hipError_t launch_dense_merge(const float* ss, const int64_t* si, int nq_grid, int k,
                               const int32_t* count, const float* cand_s, const uint32_t* cand_i,
-                              int64_t cap, const int32_t* qsel, float* out_s, int64_t* out_i,
-                              float* theta, int64_t* tie, int32_t* ctrl_out, int32_t* qlist_out,
-                              hipStream_t stream) {
+                              int64_t cap, const int32_t* qsel, const int32_t* m_dev,
+                              float* out_s, int64_t* out_i, float* theta, int64_t* tie,
+                              int32_t* n_queued, int32_t* qlist_out, unsigned long long* prefix,
+                              uint32_t* remaining, hipStream_t stream) {
   if (k < 1 || k > kMergeMaxK || nq_grid < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(dense_zero_ctrl_kernel, dim3(1), dim3(1), 0, stream, ctrl_out);
   hipLaunchKernelGGL(dense_merge_kernel, dim3((unsigned)nq_grid), dim3(kMergeThreads), 0, stream,
-                     ss, si, k, count, cand_s, cand_i, cap, qsel, out_s, out_i, theta, tie,
-                     ctrl_out, qlist_out);
+                     ss, si, k, count, cand_s, cand_i, cap, qsel, m_dev, out_s, out_i, theta, tie,
+                     n_queued, qlist_out, prefix, remaining);
   return hipGetLastError();
 }
 
-hipError_t launch_dense_repair_prep(const uint16_t* q, int dim, const int32_t* qlist, int m,
-                                    uint16_t* qc, int32_t* count, hipStream_t stream) {
-  if (m < 1) return hipSuccess;
-  const int blocks = m < 1024 ? m : 1024;
-  hipLaunchKernelGGL(dense_repair_prep_kernel, dim3(blocks), dim3(256), 0, stream, q, dim, qlist,
-                     m, qc, count);
+hipError_t launch_dense_fallback_prep(const uint16_t* q, int dim, const int32_t* qlist,
+                                      const int32_t* m_dev, uint16_t* qc, uint32_t* hist,
+                                      int n_cu, hipStream_t stream) {
+  hipLaunchKernelGGL(dense_fallback_prep_kernel, dim3((unsigned)(n_cu > 0 ? n_cu : 256)),
+                     dim3(256), 0, stream, q, dim, qlist, m_dev, qc, hist);
+  return hipGetLastError();
+}
+
+hipError_t launch_dense_radix(const int32_t* m_dev, const int32_t* qlist, int nq_grid, int shift,
+                              const float* ss, const int64_t* si, int k, uint32_t* hist,
+                              unsigned long long* prefix, uint32_t* remaining, float* theta,
+                              int64_t* tie, int32_t* count, hipStream_t stream) {
+  hipLaunchKernelGGL(dense_radix_kernel, dim3((unsigned)nq_grid), dim3(256), 0, stream, m_dev,
+                     qlist, shift, ss, si, k, hist, prefix, remaining, theta, tie, count);
   return hipGetLastError();
 }
 

@@ -122,28 +122,62 @@ inline DensePlan dense_plan(int64_t n, int k) {
   }
   return p;
 }
-constexpr int kDenseMaxRepairs = 16;
 
-// Scores of queries q[0 .. nqa) (fp16 [nqa, dim]) against rows [r0, r1) of x.  Store mode
-// (filter = false) writes them to scores[q * ld + (r - r0)]; filter mode appends (score, row)
-// to the list of global query g = qmap ? qmap[q] : q when the score beats (theta[g], tie[g]).
-hipError_t launch_dense_gemm(bool filter, const uint16_t* q, int nqa, const int32_t* qmap,
-                             const uint16_t* x, int64_t r0, int64_t r1, int dim, float* scores,
-                             int64_t ld, const float* theta, const int64_t* tie, int32_t* count,
-                             float* cand_s, uint32_t* cand_i, int64_t cap, hipStream_t stream);
-// theta[q] = ss[q, k-1], tie[q] = -1, count[q] = 0.
+// One GEMM launch of dense_ip_topk: the scores of queries q[0 .. nqa) (fp16 [nqa, dim])
+// against rows [r0, r1) of x, consumed by the epilogue's mode:
+//   0 store:     scores[q * ld + (r - r0)];
+//   1 filter:    (score, row) appended to the candidate list of global query
+//                g = qmap ? qmap[q] : q when its key is >= the bound (theta[g], tie[g]), i.e.
+//                score > theta or (score == theta and row <= tie);
+//   2 histogram: for every key >= the bound whose bits above byte `shift / 8` equal
+//                prefix[g], bin (key >> shift) & 255 of hist[q] is incremented
+//                (key = score key << 32 | ~row).
+// With m_dev the launch is a persistent grid over the *m_dev queries (read on the device; qmap
+// required; nqa unused), narrow tiles, filter or histogram mode.
+struct DenseGemm {
+  int mode;
+  const uint16_t* q;
+  int nqa;
+  const int32_t* qmap;
+  const int32_t* m_dev;
+  const uint16_t* x;
+  int64_t r0, r1;
+  int dim;
+  float* scores;
+  int64_t ld;
+  const float* theta;
+  const int64_t* tie;
+  int32_t* count;
+  float* cand_s;
+  uint32_t* cand_i;
+  int64_t cap;
+  uint32_t* hist;
+  const unsigned long long* prefix;
+  int shift;
+};
+hipError_t launch_dense_gemm(const DenseGemm& g, int n_cu, hipStream_t stream);
+// theta[q] = ss[q, k-1], tie[q] = -1, count[q] = 0; *n_queued = 0.
 hipError_t launch_dense_init(const float* ss, int nq, int k, float* theta, int64_t* tie,
-                             int32_t* count, hipStream_t stream);
-// Final top-k of (sample top-k) U (candidates) for queries qsel[0 .. nq_grid) (or 0 .. nq_grid
-// when qsel is null); *ctrl_out / qlist_out receive the queries whose lists overflowed.
+                             int32_t* count, int32_t* n_queued, hipStream_t stream);
+// Final top-k of (sample top-k) U (candidates) for queries 0 .. nq_grid (qsel null) or queued
+// queries qsel[b], b < *m_dev (m_dev non-null).  With n_queued non-null, queries whose lists
+// overflowed are appended to qlist_out (their bound raised, radix state reset).
 hipError_t launch_dense_merge(const float* ss, const int64_t* si, int nq_grid, int k,
                               const int32_t* count, const float* cand_s, const uint32_t* cand_i,
-                              int64_t cap, const int32_t* qsel, float* out_s, int64_t* out_i,
-                              float* theta, int64_t* tie, int32_t* ctrl_out, int32_t* qlist_out,
-                              hipStream_t stream);
-// Gathers the m queued queries' rows into qc and empties their lists.
-hipError_t launch_dense_repair_prep(const uint16_t* q, int dim, const int32_t* qlist, int m,
-                                    uint16_t* qc, int32_t* count, hipStream_t stream);
+                              int64_t cap, const int32_t* qsel, const int32_t* m_dev,
+                              float* out_s, int64_t* out_i, float* theta, int64_t* tie,
+                              int32_t* n_queued, int32_t* qlist_out, unsigned long long* prefix,
+                              uint32_t* remaining, hipStream_t stream);
+// The *m_dev queued queries' rows gathered into qc [m, dim]; their histograms zeroed.
+hipError_t launch_dense_fallback_prep(const uint16_t* q, int dim, const int32_t* qlist,
+                                      const int32_t* m_dev, uint16_t* qc, uint32_t* hist,
+                                      int n_cu, hipStream_t stream);
+// One byte (at `shift`) of the exact radix select of each queued query's k-th key; at shift 0
+// the bound becomes that key and the list is emptied.
+hipError_t launch_dense_radix(const int32_t* m_dev, const int32_t* qlist, int nq_grid, int shift,
+                              const float* ss, const int64_t* si, int k, uint32_t* hist,
+                              unsigned long long* prefix, uint32_t* remaining, float* theta,
+                              int64_t* tie, int32_t* count, hipStream_t stream);
 
 // Semantic chunking (chunking.hip): cos_out [n] (NaN at paper starts), seg [n] segment ids,
 // *n_seg the segment count; cnt [chunk_ranges(n)] int32 and base [chunk_ranges(n)] int64 are

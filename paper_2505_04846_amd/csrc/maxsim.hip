@@ -20,7 +20,11 @@
 //     which the workgroup stages through LDS (double-buffered, one stage in flight).  Workgroups
 //     sharing a document range are mapped onto the same XCD and start together, so the range is
 //     read from HBM about once per XCD and served from its L2 to every query group: the tile
-//     loads are ordinary (L2-allocating) loads, not streaming ones.
+//     loads are ordinary (L2-allocating) loads, not streaming ones.  Ranges are short enough
+//     (at most 262,144 tokens) that those workgroups stay within L2 reach of each other.
+//   * Software pipeline.  Each tile's epilogue (the fold of its 16 values per lane into the
+//     running maximum) is issued inside the next tile's MFMA stream, block by block, in the
+//     shadow of the MFMA before it.
 //   * K permutation.  Lane half h = l / 32 of step s carries contraction indices
 //     16 s + 8 h .. 16 s + 8 h + 7 for both operands; A and B use the same rule, so every
 //     product pairs matching indices whatever order the hardware reduces them in.
@@ -31,52 +35,58 @@ namespace msim {
 
 namespace {
 
-// LDS geometry of one 32-token tile: rows of KS*32 bytes holding 16-byte chunks at
-// XOR-swizzled positions, so that the 16 lanes of a read phase (16 different rows, one chunk
-// index) hit 16 different bank groups; a stage holds kTps tiles (16 KiB at dim 128, where the
-// staging registers and LDS must leave room for two or three resident workgroups per CU).
+// LDS geometry of one 32-token tile: rows of KS*32 bytes padded by 16, so that the A fragment
+// of k-step s of a lane sits at a fixed offset 32 s from a per-lane base (immediate offsets, no
+// per-read address arithmetic) and the 16 rows of a read phase start 16 bytes apart modulo the
+// 256-byte bank width (conflict-free); a stage holds kTps tiles.
 template <int KS>
 struct TileGeom {
   static constexpr int kCpr = KS * 2;              // 16-byte chunks per row
-  static constexpr int kRowB = KS * 32;            // bytes per row
+  static constexpr int kRowB = KS * 32 + 16;       // bytes per (padded) row
   static constexpr int kTileB = 32 * kRowB;        // bytes per tile
-  static constexpr int kTps = KS >= 8 ? 2 : 8;     // tiles per stage
-  static constexpr int kUnitsPerTile = 32 * kCpr;  // 16-byte units per tile
-  static constexpr int kSwz = kCpr < 16 ? kCpr - 1 : 15;
+  static constexpr int kTps = KS >= 8 ? 2 : 4;     // tiles per stage
 };
 
 
 // Waves per SIMD the register allocation of the score kernel must allow: two (up to 256 VGPRs),
-// which leaves the dim-128 variant room for 128 query slots per wave (measured 7-10 % faster
-// than 64 slots at three waves per SIMD: half the LDS operand reads per MFMA and half the query
-// groups, hence half the document-range re-reads).  Fewer query slots (small nq: NB = 1 or 2
-// blocks per wave) need fewer registers, and the allocation allows three or four waves per
-// SIMD: the kernel is then bound by the store stream, which more resident workgroups keep in
-// flight.
+// which leaves the dim-128 variant room for 128 query slots per wave (half the LDS operand
+// reads per MFMA of 64 slots and half the query groups, hence half the document-range
+// re-reads).  Fewer query slots (small nq: NB = 1 or 2 blocks per wave) need fewer registers,
+// and the allocation allows three or four waves per SIMD: the kernel is then bound by the
+// store stream, which more resident workgroups keep in flight.
 constexpr int maxsim_waves(int ks, int nb) {
-  if (ks == 4 || ks == 16) return 2;  // their 64 KiB of stages fit two workgroups per CU anyway
+  if (ks == 16) return 2;
   return nb >= 4 ? 2 : nb == 2 ? 3 : 4;
 }
-// Workgroups per CU: the register bound above, and the LDS of two stages (plus under 4 KiB of
-// result buffers) against the CU's 160 KiB.
+// Workgroups per CU: the register bound above, and the LDS of two stages plus the result
+// buffers against the CU's 160 KiB.
 constexpr int maxsim_resident(int ks, int nb) {
-  const int stage = (ks >= 8 ? 2 : 8) * 32 * ks * 32;
+  const int stage = (ks >= 8 ? 2 : 4) * 32 * (ks * 32 + 16);
   const int by_lds = (160 * 1024) / (2 * stage + 4096);
   const int waves = maxsim_waves(ks, nb);
   return waves < by_lds ? waves : by_lds;
 }
 
 // MaxSim scores only (the retrieval path).
+//
+// Per tile: the NB x KS MFMAs, and the epilogue of the previous tile (each block's 16 values
+// folded into its running maximum by eight v_max3) interleaved with them: block b's
+// epilogue is issued just before block b's first MFMA of the new tile, in the shadow of the
+// MFMA before it (sched_group_barrier), so no second accumulator set is needed.  When the
+// previous tile ended its document, the document's scores are reduced (maximum over the
+// half-waves, sum over each query's slots) after the new tile's MFMAs are issued.
 template <int KS, int NB, int WPW>
 __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB))) void maxsim_kernel(
     MaxsimArgs a, const int64_t* __restrict__ off, const int64_t* __restrict__ part) {
   using G = TileGeom<KS>;
   constexpr int kThreads = 64 * WPW;
   constexpr int kSlotsWG = WPW * NB * 32;
-  __shared__ __attribute__((aligned(16))) unsigned char lds[2][G::kTps * G::kTileB];
-  // Per-document results of a stage, written to HBM after the following stage's compute loop
-  // (no global stores inside the compute loop), one slot per query of the workgroup.
-  __shared__ float res_score[2][G::kTps][kSlotsWG / 32];
+  constexpr int kTps = G::kTps;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[2][kTps * G::kTileB];
+  // Per-document results, written to HBM after the barrier that follows the epilogue (a tile's
+  // epilogue runs in the next tile's step, possibly in the next stage): a ring of three
+  // stages, one slot per (tile, query of the workgroup).
+  __shared__ float res_score[3][kTps][kSlotsWG / 32];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -119,9 +129,6 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB))) void maxsim_kerne
       bq[b][s] = as_bf16x8(v);
     }
   }
-  // The query operands must be resident before the pipelined loop: otherwise their pending
-  // loads make the compiler wait for every load in flight (the prefetch included) at each tile.
-  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
 
   const int n_tok = (int)a.n_tok;
   // Document bounds clamped into [0, n_tok) so that even an invalid CSR cannot make a load go
@@ -155,7 +162,7 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB))) void maxsim_kerne
   constexpr int kRp = kThreads / G::kCpr;              // rows covered by one pass
   constexpr int kPpt = kRp >= 32 ? 1 : 32 / kRp;       // passes per tile
   constexpr int kTpp = kRp >= 32 ? kRp / 32 : 1;       // tiles per pass
-  constexpr int kUpt = G::kTps * kPpt / kTpp;          // units per thread per stage
+  constexpr int kUpt = kTps * kPpt / kTpp;             // units per thread per stage
   TileCursor prod;
   open_doc(prod, d_begin);
   u32x4 stage_regs[kUpt];
@@ -164,16 +171,18 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB))) void maxsim_kerne
   const int lc = tid % G::kCpr;
   const bool lok = 8 * lc < a.dim;
   const uint32_t lboff = 16u * lc;
-  for (int i = tid; i < (int)(sizeof(lds) / 16); i += kThreads)
-    reinterpret_cast<u32x4*>(&lds[0][0])[i] = u32x4{0u, 0u, 0u, 0u};
-  __syncthreads();  // the zeros land before any thread stores a tile over them
+  if (a.dim < 16 * KS) {  // chunks past dim are never stored: they must read as zeros
+    for (int i = tid; i < (int)(sizeof(lds) / 16); i += kThreads)
+      reinterpret_cast<u32x4*>(&lds[0][0])[i] = u32x4{0u, 0u, 0u, 0u};
+    __syncthreads();
+  }
   const uint32_t row_bytes = 2u * (uint32_t)a.dim;
   auto fetch_stage = [&](StageDesc& sd) {
     sd.d0 = prod.d;
     sd.t0 = prod.t;
     sd.valid = sd.last = sd.lng = 0u;
 #pragma unroll
-    for (int j = 0; j < G::kTps; ++j) {
+    for (int j = 0; j < kTps; ++j) {
       const bool ok = prod.d < d_end;
       const int r0 = ok ? prod.base + prod.t * 32 : 0;
       const uint32_t rmx = ok ? prod.len - prod.t * 32 - 1 : 0;  // later rows repeat the last
@@ -184,8 +193,8 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB))) void maxsim_kerne
           const uint32_t row = lr + kRp * p;
           const uint32_t r = row < rmx ? row : rmx;
           // Few-query variants (NB < 4) have one query group, so no other workgroup reads
-          // the range: streaming loads keep it out of L2 (nq = 1 on 26.6 GB: 4.35 -> 3.84 ms).
-          // With several groups the range is re-served from L2 and ordinary loads are faster.
+          // the range: streaming loads keep it out of L2.  With several groups the range is
+          // re-served from L2 and ordinary loads are faster.
           const char* src = tptr + (r * row_bytes + lboff);
           stage_regs[(j / kTpp) * kPpt + p] = NB < 4 ? load16_stream(src) : load16(src);
         }
@@ -193,7 +202,6 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB))) void maxsim_kerne
       if (ok) {
         sd.valid |= 1u << j;
         if (prod.t + 1 == prod.cnt) sd.last |= 1u << j;
-        if (prod.len > 65536) sd.lng |= 1u << j;
         if (++prod.t == prod.cnt) {  // advance the producer to the next tile
           if (prod.d + 1 < d_end)
             open_doc(prod, prod.d + 1);
@@ -209,8 +217,8 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB))) void maxsim_kerne
     for (int m = 0; m < kUpt; ++m) {
       const int j = (m / kPpt) * kTpp + lt;
       const uint32_t row = lr + kRp * (m % kPpt);
-      *reinterpret_cast<u32x4*>(
-          &lds[buf][j * G::kTileB + row * G::kRowB + 16 * (lc ^ (row & G::kSwz))]) = stage_regs[m];
+      *reinterpret_cast<u32x4*>(&lds[buf][j * G::kTileB + row * G::kRowB + lboff]) =
+          stage_regs[m];
     }
   };
 
@@ -219,62 +227,69 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB))) void maxsim_kerne
 #pragma unroll
   for (int b = 0; b < NB; ++b) rm[b] = -__builtin_huge_valf();
   const int n_wg_q = (a.nq - qwg) < WPW * a.qpw ? (a.nq - qwg) : WPW * a.qpw;
-
-  // ---- consumer: the 32-token tiles of one stage
-  auto compute_stage = [&](const StageDesc& sd, int buf) {
-#pragma unroll 1
-    for (int j = 0; j < G::kTps; ++j) {
-      if (!((sd.valid >> j) & 1u)) break;  // uniform
-      const bool last = (sd.last >> j) & 1u;
-      if (wave_active) {
-        // A operand: tile row `col`, k chunk 2 s + half (swizzled position in LDS), read one
-        // k-step ahead of its MFMAs
-        const unsigned char* tile = &lds[buf][j * G::kTileB + col * G::kRowB];
-        auto read_a = [&](int s) {
-          const int c = 2 * s + half;
-          return as_bf16x8(*reinterpret_cast<const u32x4*>(tile + ((c ^ (col & G::kSwz)) * 16)));
-        };
-        f32x16 acc[NB];
-#pragma unroll
-        for (int b = 0; b < NB; ++b)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) acc[b][r] = 0.f;
-        bf16x8 av = read_a(0);
-#pragma unroll
-        for (int s = 0; s < KS; ++s) {
-          const bf16x8 an = s + 1 < KS ? read_a(s + 1) : av;
-#pragma unroll
-          for (int b = 0; b < NB; ++b)
-            acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bq[b][s], acc[b], 0, 0, 0);
-          av = an;
-        }
-#pragma unroll
-        for (int b = 0; b < NB; ++b) {
-          float m = fmaxf(acc[b][0], acc[b][1]);  // this tile's maximum over the lane's rows
-#pragma unroll
-          for (int r = 2; r < 16; r += 2) m = fmaxf(fmaxf(m, acc[b][r]), acc[b][r + 1]);
-          rm[b] = fmaxf(rm[b], m);
-        }
-        if (last) {  // last tile of the document: reduce over half-waves and slots, emit
-          float qs = 0.f;
-#pragma unroll
-          for (int b = 0; b < NB; ++b) {
-            const float m = fmaxf(rm[b], __shfl_xor(rm[b], 32));
-            rm[b] = -__builtin_huge_valf();
-            const float v = half32_sum(slot_row[b] >= 0 ? m : 0.f);
-            if ((my_blocks >> b) & 1u) qs += v;
-          }
-          if (lane < a.qpw) res_score[buf][j][wave * a.qpw + lane] = qs;
-        }
-      }
-    }
+  const uint32_t a_lane = (uint32_t)(col * G::kRowB + half * 16);  // A: row col, chunk half
+  auto frag = [&](int buf, int j, int s) {
+    return as_bf16x8(
+        *reinterpret_cast<const u32x4*>(&lds[buf][j * G::kTileB] + a_lane + 32 * s));
   };
 
-  // Results of the documents that ended in stage buffer `rb` -> HBM (coalesced per document).
+  f32x16 acc[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[b][r] = -__builtin_huge_valf();
+  // One tile: its MFMAs into acc, and the previous tile's epilogue (acc folded into rm) issued
+  // block by block just before the block's first MFMA of this tile.  fr[0] holds the tile's
+  // k-step 0 fragment on entry and the next tile's (when in the same stage) on exit.
+  auto step = [&](int buf, int j, bf16x8 (&fr)[2]) {
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      // the fragment of the next k-step (of the next tile after the last one, same stage)
+      if (s + 1 < KS)
+        fr[(s + 1) & 1] = frag(buf, j, s + 1);
+      else if (j + 1 < kTps)
+        fr[(s + 1) & 1] = frag(buf, j + 1, 0);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        if (s == 0) {  // eight v_max3 folding the 16 values into rm
+          float m = rm[b];
+#pragma unroll
+          for (int r = 0; r < 16; r += 2) m = fmaxf(fmaxf(m, acc[b][r]), acc[b][r + 1]);
+          rm[b] = m;
+        }
+        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[s & 1], bq[b][s],
+                                                         s == 0 ? f32x16{} : acc[b], 0, 0, 0);
+      }
+      if (s + 1 < KS || j + 1 < kTps) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        if (s == 0) __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);  // VALU
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                      // MFMA
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  // The end of a document whose last tile's epilogue has run: maximum over the two half-waves
+  // (rows), sum over the slots of each query in a fixed order, into LDS slot (rb, j).
+  auto doc_end = [&](int rb, int j) {
+    float qs = 0.f;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(rm[b]),
+                                                       __float_as_uint(rm[b]), false, false);
+      const float m = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+      rm[b] = -__builtin_huge_valf();
+      const float v = half32_sum(slot_row[b] >= 0 ? m : 0.f);
+      if ((my_blocks >> b) & 1u) qs += v;
+    }
+    if (lane < a.qpw) res_score[rb][j][wave * a.qpw + lane] = qs;
+  };
+
+  // Results of the documents that ended in a stage (ring slot rb) -> HBM (coalesced per doc).
   auto write_results = [&](const StageDesc& sd, int rb) {
     int d = sd.d0;
 #pragma unroll 1
-    for (int j = 0; j < G::kTps; ++j) {
+    for (int j = 0; j < kTps; ++j) {
       if (!((sd.valid >> j) & 1u)) break;
       if ((sd.last >> j) & 1u) {
         if (tid < n_wg_q) a.scores[(int64_t)(qwg + tid) * a.n_docs + d] = res_score[rb][j][tid];
@@ -283,29 +298,63 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB))) void maxsim_kerne
     }
   };
 
-  StageDesc cur, nxt, prv;
+  StageDesc cur, nxt, prv, prv2;
   fetch_stage(cur);
+  // The query operands and the first stage land together.  The operands must be resident
+  // before the pipelined loop: otherwise their pending loads make the compiler wait for every
+  // load in flight (the prefetch included) at each tile.
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
   store_stage(0);
   __syncthreads();
+  bf16x8 fr[2];
+  fr[0] = frag(0, 0, 0);
 
-  for (int stage = 0;; ++stage) {
+  // Pipeline state (uniform): whether the tile whose epilogue runs next ends its document, and
+  // where that document's result goes.  (The first tile's "previous tile" is acc = -inf, whose
+  // epilogue changes nothing: one code path, whose registers fit without spills.)
+  bool pend_last = false;
+  int pend_rb = 0, pend_j = 0;
+  int stage = 0;
+  for (;; ++stage) {
     const int buf = stage & 1;
+    const int rb = stage % 3;
     const bool more = prod.d < d_end;
     if (more) fetch_stage(nxt);  // global loads in flight while this stage is computed
-    compute_stage(cur, buf);
-    // the previous stage's results (complete since the last barrier)
-    if (stage > 0) write_results(prv, buf ^ 1);
+    if (wave_active) {
+#pragma unroll
+      for (int j = 0; j < kTps; ++j) {
+        if (!((cur.valid >> j) & 1u)) break;  // uniform: only the final stage is partial
+        step(buf, j, fr);
+        if (pend_last) doc_end(pend_rb, pend_j);
+        pend_last = (cur.last >> j) & 1u;
+        pend_rb = rb;
+        pend_j = j;
+      }
+    }
+    if (stage >= 2) write_results(prv2, (stage - 2) % 3);
     if (more) store_stage(buf ^ 1);
     __syncthreads();
-    if (!more) {
-      write_results(cur, buf);
-      break;
-    }
+    if (!more) break;
+    fr[0] = frag(buf ^ 1, 0, 0);
+    prv2 = prv;
     prv = cur;
     cur = nxt;
   }
+  // the last computed tile's epilogue and document end, then the final two stages' results
+  if (wave_active) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      float m = fmaxf(acc[b][0], acc[b][1]);
+#pragma unroll
+      for (int r = 2; r < 16; r += 2) m = fmaxf(fmaxf(m, acc[b][r]), acc[b][r + 1]);
+      rm[b] = fmaxf(rm[b], m);
+    }
+    if (pend_last) doc_end(pend_rb, pend_j);
+  }
+  __syncthreads();
+  if (stage >= 1) write_results(prv, (stage - 1) % 3);
+  write_results(cur, stage % 3);
 }
-
 
 __global__ void partition_kernel(const int64_t* off, int64_t n_docs, int64_t n_tok, int R,
                                  int64_t* part, int32_t* ctrl, int n_ctrl) {
@@ -379,6 +428,8 @@ hipError_t launch_variant(const MaxsimPlan& plan, const MaxsimArgs& args, bool a
 
 using namespace msim;
 
+constexpr int64_t kMaxRangeTokens = 262144;  // 64 MiB of bf16 tokens at dim 128
+
 bool maxsim_plan(int nq, int lq, int64_t n_docs, int64_t n_tok, int dim, bool argmax, int n_cu,
                  MaxsimPlan* p) {
   if (dim < 8 || dim > 256 || dim % 8 != 0 || lq < 1 || nq < 1 || n_docs < 1) return false;
@@ -406,6 +457,14 @@ bool maxsim_plan(int nq, int lq, int64_t n_docs, int64_t n_tok, int dim, bool ar
   const int occ = argmax ? msim::argmax_resident(p->ks) : msim::maxsim_resident(p->ks, p->nb);
   const int64_t target_wg = (int64_t)(n_cu > 0 ? n_cu : 256) * occ * (argmax ? 1 : 32);
   int64_t R = (target_wg + p->n_qgroups - 1) / p->n_qgroups;
+  // ... and, for the score kernel, ranges of at most kMaxRangeTokens tokens: the up to 64
+  // workgroups of an XCD that read one range together drift apart over a long range, after
+  // which its tiles are fetched again from beyond the XCD's L2 (a 7-million-token range at
+  // 4,096 x 64 queries fetched ~195x the store per launch)
+  if (!argmax) {
+    const int64_t by_len = (n_tok + kMaxRangeTokens - 1) / kMaxRangeTokens;
+    if (R < by_len) R = by_len;
+  }
   const int64_t max_by_tokens = n_tok / 1024 > 0 ? n_tok / 1024 : 1;
   if (R > max_by_tokens) R = max_by_tokens;
   if (R > n_docs) R = n_docs;

@@ -3,7 +3,9 @@
 The call has three regimes, each covered here:
   * the store is no larger than the exact sample (every row is scored and selected directly);
   * the filter path: rows past the sample are kept only when they beat the sample's k-th score;
-  * the repair path: a query whose candidate list overflows is rescanned with a raised bound.
+  * the exact fallback: a query whose candidate list overflows is queued on the device and its
+    k-th key found by a radix select over rescans of the store, then its top-k collected; the
+    call stays asynchronous (it is captured and replayed in a HIP graph here).
 Top-k lists are checked with the rules of tests/topk_check.py at tolerance 2e-3 (fp16 products
 are exact in fp32, so scores differ from the oracle only by the fp32 summation order).
 """
@@ -95,7 +97,7 @@ def test_dense_topk_filter_path_few_queries():
         check_topk(s[q], i[q], O[q], k, rel=REL)
 
 
-def test_dense_topk_overflowing_lists_are_repaired():
+def test_dense_topk_overflowing_lists_take_the_exact_fallback():
     nq, n, dim, k = 40, 150_000, 64, 20
     Q, X = _rows(nq, dim, 21), _rows(n, dim, 22)
     a0 = SAMPLE_ROWS + 100
@@ -117,6 +119,63 @@ def test_dense_topk_overflowing_lists_are_repaired():
     assert abs(s[0, 0] - O[0, a0]) <= REL * abs(O[0, a0])
     for q in range(2, 4):
         check_topk(s[q], i[q], O[q], k, rel=REL)
+
+
+def _overflowing_store(nq, n, dim, copies, seed):
+    # queries near a common direction u; `copies` bit-identical rows equal to u past the sample
+    # outscore every random row for every query, so every candidate list overflows
+    g = torch.Generator().manual_seed(seed)
+    u = synth.unit_rows(1, dim, g, "cpu", torch.float32)
+    noise = torch.randn((nq, dim), generator=g)
+    Q = synth._normalise(u + 0.1 * noise / dim ** 0.5).to(torch.float16)
+    X = _rows(n, dim, seed + 1)
+    a0 = SAMPLE_ROWS + 777
+    X[a0:a0 + copies] = u.to(torch.float16)
+    return Q, X, a0
+
+
+def test_dense_topk_every_list_overflows():
+    # 70 queries: the scan takes the wide tile, the fallback two 64-query tiles
+    nq, n, dim, k = 70, 140_000, 64, 100
+    Q, X, a0 = _overflowing_store(nq, n, dim, 2500, 41)
+    s, i = hpr.dense_ip_topk(Q.to(DEV), X.to(DEV), k)
+    s, i = s.cpu().numpy(), i.cpu().numpy()
+    _check_structure(s, i, n, k)
+    for q in range(nq):
+        assert i[q].tolist() == list(range(a0, a0 + k)), f"query {q}"
+        assert np.all(s[q] == s[q, 0])
+    Qh, Xh = _f16(Q), _f16(X)
+    O = oracle.dense_scores(Qh[[0, 63, 64, 69]], Xh)
+    for r, q in enumerate((0, 63, 64, 69)):
+        check_topk(s[q], i[q], O[r], k, rel=REL)
+
+
+def test_dense_topk_replays_in_a_hip_graph_with_overflow():
+    # the whole call, the device-decided fallback included, is captured once and replayed with
+    # eager work and synchronisation in between; every replay reproduces the eager result
+    nq, n, dim, k = 40, 150_000, 64, 20
+    Q, X = _rows(nq, dim, 21), _rows(n, dim, 22)
+    a0 = SAMPLE_ROWS + 100
+    X[a0:a0 + 3000] = Q[0]
+    Qd, Xd = Q.to(DEV), X.to(DEV)
+    ref_s, ref_i = hpr.dense_ip_topk(Qd, Xd, k)
+    ws = hpr.dense_workspace(Qd, Xd, k)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        hpr.dense_ip_topk(Qd, Xd, k, ws=ws)
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        gs, gi = hpr.dense_ip_topk(Qd, Xd, k, ws=ws)
+    for rep in range(3):
+        gs.fill_(float("nan"))
+        gi.fill_(-1)
+        g.replay()
+        hpr.dense_ip_topk(Qd[:3].contiguous(), Xd, 5)   # unrelated eager work
+        torch.cuda.synchronize()
+        assert torch.equal(gs, ref_s) and torch.equal(gi, ref_i), f"replay {rep}"
+    assert gi[0].tolist() == list(range(a0, a0 + k))
 
 
 def test_dense_topk_planted_rows_rank_first():

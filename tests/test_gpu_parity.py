@@ -467,6 +467,37 @@ def test_calls_on_a_non_default_stream():
     assert torch.equal(ref, out)
 
 
+def test_concurrent_calls_on_two_streams_with_separate_workspaces():
+    # two streams, each with its own workspace, run different calls at the same time; the
+    # results equal those of the same calls made one after the other on the default stream
+    w1 = synth.tiny_maxsim(seed=7, n_docs=3000, ld=48)
+    c = synth.coltrast_step(seed=8, nq=16, n_neg=7, ld=64)
+    Q1, D1, off1 = _to_dev(w1["Q"], w1["D"], w1["off"])
+    Q2, D2, off2, pos2 = _to_dev(c["Q"], c["D"], c["off"], c["pos"])
+    ref_s, ref_i = hpr.maxsim_topk(Q1, D1, off1, 50)
+    ref_l = hpr.coltrast_loss_fwd_bwd(Q2, D2, off2, pos2, 1.5625)
+    ref_sc = hpr.maxsim_score(Q2, D2, off2)
+    torch.cuda.synchronize()
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    ws_a = torch.empty(hpr.lib().maxsim_topk_workspace_size(8, 32, 3000, D1.shape[0], 128, 50),
+                       dtype=torch.uint8, device=DEV)
+    ws_b = hpr.coltrast_workspace(Q2, D2, off2)
+    outs = []
+    for rep in range(3):
+        with torch.cuda.stream(sa):
+            ta = hpr.maxsim_topk(Q1, D1, off1, 50, ws=ws_a)
+            sc = hpr.maxsim_score(Q2, D2, off2)
+        with torch.cuda.stream(sb):
+            lb = hpr.coltrast_loss_fwd_bwd(Q2, D2, off2, pos2, 1.5625, ws=ws_b)
+        outs.append((ta, sc, lb))
+    torch.cuda.synchronize()
+    for ta, sc, lb in outs:
+        assert torch.equal(ta[0], ref_s) and torch.equal(ta[1], ref_i)
+        assert torch.equal(sc, ref_sc)
+        for key in ("loss", "dq", "dd"):
+            assert torch.equal(lb[key], ref_l[key]), key
+
+
 def test_csr_validate():
     good = torch.tensor([0, 3, 4, 9], dtype=torch.int64, device=DEV)
     assert hpr.csr_validate(good, 9) == ("HPR_OK", -1)
