@@ -3,6 +3,8 @@
     python -m paper_2505_04846_amd.prof_summary stats  DIR  OUT.md  --title T --command C
     python -m paper_2505_04846_amd.prof_summary traffic FETCH_DIR WRITE_DIR --kernel NAME
         --match SUBSTRING --workload W --sources a.hip,b.h --command C [--json profiles/traffic.json]
+    python -m paper_2505_04846_amd.prof_summary counters DIR [DIR ...] --out OUT.md
+        --match SUBSTRING --title T --command C [--command C ...]
 
 `stats` renders run_kernel_stats.csv of a `rocprofv3 --kernel-trace --stats` run as a markdown
 table.  `traffic` reads two `rocprofv3 --pmc` runs (FETCH_SIZE, then WRITE_SIZE; KiB per
@@ -10,7 +12,8 @@ dispatch) of a program that first copied 256 MiB device to device (bench.py
 --copy-calibration): the copy's readings give the scale of each counter (known bytes / reading),
 and the scaled per-dispatch HBM bytes of the kernels whose name contains SUBSTRING are recorded
 in traffic.json under (kernel, workload, source hash) -- bench.py reports them only while the
-kernel sources are unchanged.
+kernel sources are unchanged.  `counters` renders `rocprofv3 --pmc` runs of MFMA, clock, LDS and
+L2 counters as raw means and derived figures (clock, MFMA busy fraction, executed FLOP/s).
 """
 
 import argparse
@@ -97,6 +100,67 @@ def traffic(args):
     print(json.dumps(rec))
 
 
+def _agent(d):
+    """(XCD count, SIMD count) of the GPU agent of a rocprofv3 run."""
+    for r in _csv(d, "*agent_info.csv"):
+        if r.get("Agent_Type", "").upper().endswith("GPU") or r.get("Name", "").startswith("gfx"):
+            return int(r["Num_Xcc"]), int(r["Simd_Count"])
+    raise SystemExit(f"no GPU agent in {d}")
+
+
+def counters(args):
+    """Derived MFMA / clock / LDS / L2 figures of the dispatches matching --match, from one or
+    more `rocprofv3 --pmc` runs (each run's counters are averaged over its matching dispatches;
+    every run must have collected GRBM_GUI_ACTIVE, which sums the busy cycles of all XCDs)."""
+    merged, durs = {}, []
+    n_xcc = n_simd = None
+    for d in args.dirs:
+        n_xcc, n_simd = _agent(d)
+        rows = [r for r in _csv(d, "*counter_collection.csv") if args.match in r["Kernel_Name"]]
+        if not rows:
+            raise SystemExit(f"no dispatch of {args.match} in {d}")
+        per = {}
+        for r in rows:
+            per.setdefault(r["Dispatch_Id"], {})[r["Counter_Name"]] = float(r["Counter_Value"])
+            per[r["Dispatch_Id"]]["_ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+        disp = list(per.values())
+        for name in disp[0]:
+            if not name.startswith("_"):
+                merged.setdefault(name, []).append(statistics.mean(x[name] for x in disp))
+        durs += [x["_ns"] * 1e-9 for x in disp]
+    c = {k: statistics.mean(v) for k, v in merged.items()}
+    dur = statistics.mean(durs)
+    lines = [f"# {args.title}", "", "Commands (one `rocprofv3 --pmc` run each):", "", "```"]
+    lines += args.command + ["```", "", f"Dispatches of `{args.match}`: mean duration "
+                             f"{dur * 1e3:.3f} ms.", "", "| counter | mean per dispatch |",
+                             "|---|---:|"]
+    lines += [f"| `{k}` | {v:.6g} |" for k, v in sorted(c.items())]
+    lines += ["", "Derived (per dispatch; XCDs and SIMDs from the run's agent record: "
+              f"{n_xcc} and {n_simd}):", ""]
+    cyc = c.get("GRBM_GUI_ACTIVE", 0.0) / n_xcc  # busy cycles of one XCD
+    if cyc:
+        lines.append(f"- clock: GRBM_GUI_ACTIVE / {n_xcc} / duration = {cyc / dur / 1e9:.3f} GHz")
+    if cyc and "SQ_VALU_MFMA_BUSY_CYCLES" in c:
+        lines.append(f"- MFMA busy: SQ_VALU_MFMA_BUSY_CYCLES / (cycles x {n_simd} SIMDs) = "
+                     f"{c['SQ_VALU_MFMA_BUSY_CYCLES'] / (cyc * n_simd):.3f}")
+    mops = sum(c.get(k, 0.0) for k in ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_INSTS_VALU_MFMA_MOPS_F16"))
+    if mops:
+        lines.append(f"- executed matrix FLOP/s: MOPS x 512 / duration = {mops * 512 / dur / 1e12:.1f} "
+                     f"TFLOP/s ({mops * 512:.4g} FLOP per dispatch)")
+    if c.get("SQ_INSTS_MFMA"):
+        m = c["SQ_INSTS_MFMA"]
+        if "SQ_INSTS_VALU" in c:
+            lines.append(f"- other VALU instructions per MFMA: {(c['SQ_INSTS_VALU'] - m) / m:.2f}")
+        if "SQ_INSTS_LDS" in c:
+            lines.append(f"- LDS instructions per MFMA: {c['SQ_INSTS_LDS'] / m:.3f}")
+    if "TCC_HIT_sum" in c and "TCC_MISS_sum" in c:
+        h, mi = c["TCC_HIT_sum"], c["TCC_MISS_sum"]
+        lines.append(f"- L2 hit rate: {h / (h + mi):.3f} ({mi:.4g} misses)")
+    with open(args.out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines[-8:]))
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -114,8 +178,14 @@ def main():
     b.add_argument("--sources", required=True)
     b.add_argument("--command", required=True)
     b.add_argument("--json", default=os.path.join(ROOT, "profiles", "traffic.json"))
+    c = sub.add_parser("counters")
+    c.add_argument("dirs", nargs="+")
+    c.add_argument("--out", required=True)
+    c.add_argument("--match", required=True)
+    c.add_argument("--title", required=True)
+    c.add_argument("--command", action="append", required=True)
     args = ap.parse_args()
-    (stats if args.cmd == "stats" else traffic)(args)
+    {"stats": stats, "traffic": traffic, "counters": counters}[args.cmd](args)
 
 
 if __name__ == "__main__":
