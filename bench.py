@@ -64,6 +64,12 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the extra HIP-graph replay timing of the same step")
+    ap.add_argument("--cpu-subset", action="store_true",
+                    help="instead of the GPU timing: the fp64 oracle on this host over the whole "
+                         "store for a query subset (li_retrieval 32 queries, li_large 8, "
+                         "dense_retrieval 16 of which 8 planted), its time measured and "
+                         "extrapolated to every query, and the GPU top-k of those queries "
+                         "compared with the oracle's")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 256 MiB device-to-device copy three times (the "
                          "reference kernel that scales rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -340,6 +346,94 @@ def build_workload(name, dev, scale, tau, nq_sub=None):
     raise SystemExit(f"workload {name} is not available in this build")
 
 
+def cpu_subset(args):
+    """The oracle over the whole store for a seeded query subset, on this host's cores.  Decoding
+    the bf16 / fp16 store to float64 (chunk by chunk: the whole store in float64 would not fit
+    the host) is input preparation and is not timed.  Prints one JSON line."""
+    import numpy as np
+    import torch
+    import oracle
+    import paper_2505_04846_amd as hpr
+    import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    name = args.workload
+    g = torch.Generator().manual_seed(5)
+    if name in ("li_retrieval", "li_large"):
+        w = (synth.li_retrieval if name == "li_retrieval" else synth.li_large)(seed=0, device=dev)
+        Q, D, off, k = w["Q"], w["D"], w["off"], w["k"]
+        nq_all = Q.shape[0]
+        m = 32 if name == "li_retrieval" else 8
+        sel = torch.cat([torch.zeros(1, dtype=torch.int64),
+                         1 + torch.randperm(nq_all - 1, generator=g)[:m - 1]]).sort().values
+        gs, gi = hpr.maxsim_topk(Q[sel.to(dev)].contiguous(), D, off, k)
+        torch.cuda.synchronize()
+        Qh = oracle.decode_bf16(Q[sel.to(dev)].cpu().view(torch.int16).numpy())
+        offh = off.cpu().numpy()
+        n_docs = offh.size - 1
+        parts, spent, d0 = [], 0.0, 0
+        chunk = 20000
+        while d0 < n_docs:
+            d1 = min(n_docs, d0 + chunk)
+            Dh = oracle.decode_bf16(D[int(offh[d0]):int(offh[d1])].cpu().view(torch.int16).numpy())
+            t0 = time.perf_counter()
+            parts.append(oracle.maxsim_scores(Qh, Dh, offh[d0:d1 + 1] - offh[d0]))
+            spent += time.perf_counter() - t0
+            d0 = d1
+            print(f"[cpu-subset] {d0}/{n_docs} documents, {spent:.0f} s of oracle time",
+                  file=sys.stderr, flush=True)
+        S = np.concatenate(parts, axis=1)
+        unit, pairs = "pairs/s", m * n_docs
+    else:
+        w = synth.dense_retrieval(seed=0, device=dev)
+        Q, X, k = w["Q"], w["X"], w["k"]
+        nq_all = Q.shape[0]
+        pq = w["planted_q"].cpu()
+        plain = torch.tensor([q for q in range(nq_all) if q not in set(pq.tolist())])
+        sel = torch.cat([pq[torch.randperm(pq.numel(), generator=g)[:8]],
+                         plain[torch.randperm(plain.numel(), generator=g)[:8]]]).sort().values
+        m = sel.numel()
+        gs, gi = hpr.dense_ip_topk(Q[sel.to(dev)].contiguous(), X, k)
+        torch.cuda.synchronize()
+        Qh = oracle.decode_fp16(Q[sel.to(dev)].cpu().view(torch.int16).numpy())
+        n = X.shape[0]
+        parts, spent, r0 = [], 0.0, 0
+        while r0 < n:
+            r1 = min(n, r0 + 65536)
+            Xh = oracle.decode_fp16(X[r0:r1].cpu().view(torch.int16).numpy())
+            t0 = time.perf_counter()
+            parts.append(oracle.dense_scores(Qh, Xh))
+            spent += time.perf_counter() - t0
+            r0 = r1
+            print(f"[cpu-subset] {r0}/{n} rows, {spent:.0f} s of oracle time", file=sys.stderr,
+                  flush=True)
+        S = np.concatenate(parts, axis=1)
+        unit, pairs = "queries/s", m
+    t0 = time.perf_counter()
+    os_, oi = oracle.rank_topk(S, k)
+    spent += time.perf_counter() - t0
+    # the GPU's lists for the same queries against the oracle: exact index sets, and the
+    # largest relative difference of a returned score from the oracle score of its index
+    gs, gi = gs.cpu().numpy().astype(np.float64), gi.cpu().numpy()
+    exact_sets = sum(int(set(gi[r].tolist()) == set(oi[r].tolist())) for r in range(m))
+    exact_order = sum(int(np.array_equal(gi[r], oi[r])) for r in range(m))
+    ref = np.take_along_axis(S, gi, axis=1)
+    rel = float(np.max(np.abs(gs - ref) / np.maximum(np.abs(ref), 1e-3)))
+    gap_tight = sum(int(os_[r, k - 1] - np.sort(S[r])[-k - 1] > 2e-3 * max(abs(os_[r, k - 1]), 1e-3))
+                    for r in range(m))
+    line = {
+        "kind": "oracle_subset", "workload": name, "queries": m, "query_ids": sel.tolist(),
+        "oracle_seconds": spent, "value": pairs / spent, "unit": unit,
+        "extrapolated_seconds_all_queries": spent * nq_all / m, "all_queries": nq_all,
+        "cores": blas_threads(), "cpu_model": cpu_model(),
+        "gpu_vs_oracle": {"exact_index_sets": exact_sets, "exact_order": exact_order,
+                          "queries_with_kth_gap_above_tolerance": gap_tight,
+                          "max_rel_score_error": rel},
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -348,6 +442,12 @@ def main():
               "(the sharding design is described in DESIGN.md); run with --gpus 1",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.cpu_subset:
+        if args.workload not in ("li_retrieval", "li_large", "dense_retrieval"):
+            raise SystemExit("--cpu-subset applies to li_retrieval, li_large and dense_retrieval")
+        cpu_subset(args)
+        return
 
     import torch
     import paper_2505_04846_amd as hpr
@@ -437,29 +537,36 @@ def main():
             kernels[name] = {"avg_us": round(1e3 * tot / n, 3), "launches": n}
     kname = W["kernel"]
     k_avg_s = kernels[kname]["avg_us"] * 1e-6
+    # a step may launch the dominant kernel several times (the persistent MaxSim grid runs one
+    # launch per pass of query groups): the work per launch is the step's share
+    per_step = kernels[kname]["launches"] / args.steps
+    per_launch = 1.0 / per_step if per_step >= 1 else 1.0
     # the dominant kernel's bound: MFMA unless its arithmetic intensity (algorithmic FLOPs per
     # algorithmic byte) is below the machine balance, 2.5 PFLOP/s / 8 TB/s = 312 FLOP/B
     hbm_bound = W.get("bytes") and W["flops"] / W["bytes"] < PEAK_BF16_TFLOPS / PEAK_HBM_GBS * 1e3
     twl = args.workload if not args.nq else f"{args.workload}_nq{args.nq}"
+    flops_l = W["flops"] * per_launch
     if hbm_bound:
-        gbs = W["bytes"] / k_avg_s / 1e9
+        bytes_l = W["bytes"] * per_launch
+        gbs = bytes_l / k_avg_s / 1e9
         roofline = {
             "bound": "hbm", "kernel": kname, "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
             "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
             "traffic": committed_traffic(kname, twl, W["sha"]),
-            "bytes_per_launch": W["bytes"], "flops_per_launch": W["flops"],
-            "avg_launch_us": kernels[kname]["avg_us"],
-            "mfma_tflops": round(W["flops"] / k_avg_s / 1e12, 2),
+            "bytes_per_launch": bytes_l, "flops_per_launch": flops_l,
+            "avg_launch_us": kernels[kname]["avg_us"], "launches_per_step": per_step,
+            "mfma_tflops": round(flops_l / k_avg_s / 1e12, 2),
             "measured_peak": round(meas_gbs, 1), "frac_of_measured": round(gbs / meas_gbs, 4),
         }
     else:
-        achieved = W["flops"] / k_avg_s / 1e12
+        achieved = flops_l / k_avg_s / 1e12
         roofline = {
             "bound": "mfma", "kernel": kname, "achieved": round(achieved, 2),
             "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
             "traffic": committed_traffic(kname, twl, W["sha"]),
-            "flops_per_launch": W["flops"], "avg_launch_us": kernels[kname]["avg_us"],
+            "flops_per_launch": flops_l, "avg_launch_us": kernels[kname]["avg_us"],
+            "launches_per_step": per_step,
             "measured_peak": round(meas_tflops, 1),
             "frac_of_measured": round(achieved / meas_tflops, 4),
         }

@@ -161,16 +161,29 @@ struct Carver {
   }
 };
 
+// Score calls: `part` is the range table, of part_bytes bytes; after its n_ranges + 1 entries
+// a persistent plan keeps its checkpoint counters (8 per pass) there when they fit.
 hpr_status run_maxsim(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d_tok,
                       const int64_t* d_off, int64_t n_docs, int64_t n_tok, int32_t dim,
                       float* scores, uint16_t* amax, int32_t* ctrl, int n_ctrl, int64_t* part,
-                      hipStream_t stream) {
+                      size_t part_bytes_avail, hipStream_t stream) {
   int n_cu = 0;
   hpr_status st = current_cu_count(&n_cu);
   if (st != HPR_OK) return st;
   MaxsimPlan plan;
   if (!maxsim_plan(nq, lq, n_docs, n_tok, dim, amax != nullptr, n_cu, &plan))
     return fail(HPR_ERR_UNSUPPORTED_SHAPE, "no MaxSim plan for this shape");
+  if (!amax && (size_t)(plan.n_ranges + 1) * sizeof(int64_t) > part_bytes_avail)
+    return fail(HPR_ERR_UNSUPPORTED_SHAPE, "%d document ranges exceed the range table",
+                plan.n_ranges);
+  if (!amax && plan.persist) {
+    const size_t used = (size_t)(plan.n_ranges + 1) * sizeof(int64_t);
+    const size_t words = (size_t)8 * maxsim_passes(plan);
+    if (used + words * sizeof(int32_t) <= part_bytes_avail) {
+      ctrl = reinterpret_cast<int32_t*>(part + plan.n_ranges + 1);
+      n_ctrl = (int)words;
+    }
+  }
   hipError_t e = hipSuccess;
   if (!amax) {  // the argmax kernel finds its own ranges (one round of workgroups)
     e = timed("partition", stream, [&] {
@@ -178,11 +191,13 @@ hpr_status run_maxsim(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t*
     });
     if (e != hipSuccess) return hip_fail(e, "partition launch");
   }
-  e = timed(amax ? "maxsim_argmax" : "maxsim", stream, [&] {
-    return launch_maxsim(plan, q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, part, scores, amax,
-                         ctrl, n_ctrl, stream);
-  });
-  if (e != hipSuccess) return hip_fail(e, "maxsim launch");
+  for (int pass = 0; pass < maxsim_passes(plan); ++pass) {
+    e = timed(amax ? "maxsim_argmax" : "maxsim", stream, [&] {
+      return launch_maxsim(plan, pass, q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, part, scores,
+                           amax, ctrl, n_ctrl, stream);
+    });
+    if (e != hipSuccess) return hip_fail(e, "maxsim launch");
+  }
   return HPR_OK;
 }
 
@@ -242,7 +257,8 @@ hpr_status run_loss(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d
   float* terms = c.take<float>((size_t)nq * sizeof(float));
   float* gq_part = c.take<float>((size_t)grad_q_ranges(n_docs, n_tok, (int64_t)nq * lq, dim) *
                                  (size_t)nq * lq * dim * sizeof(float));
-  st = run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, S, amax, ctrl, n_ctrl, nullptr, s);
+  st = run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, S, amax, ctrl, n_ctrl, nullptr, 0,
+                  s);
   if (st != HPR_OK) return st;
   const float w = total ? 0.5f : 1.0f;
   hipError_t e = timed("infonce", s, [&] {
@@ -331,7 +347,7 @@ hpr_status maxsim_score(const uint16_t* q, int32_t nq, int32_t lq, const uint16_
   Carver c(ws);
   int64_t* part = c.take<int64_t>(part_bytes(n_docs));
   return run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, scores, nullptr, nullptr, 0,
-                    part, static_cast<hipStream_t>(stream));
+                    part, part_bytes(n_docs), static_cast<hipStream_t>(stream));
 }
 
 hpr_status maxsim_score_noalloc(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t* d_tok,
@@ -353,12 +369,22 @@ hpr_status maxsim_score_noalloc(const uint16_t* q, int32_t nq, int32_t lq, const
   int64_t* part = nullptr;
   st = scratch_address(&part);
   if (st != HPR_OK) return st;
-  // The same two launches as maxsim_score (partition, then scores), without the timing events.
+  // The same launches as maxsim_score (partition, then the score passes, the checkpoint
+  // counters of a persistent plan after the range table), without the timing events.
+  int32_t* sync = nullptr;
+  int n_sync = 0;
+  if (plan.persist && ((size_t)plan.n_ranges + 1) * sizeof(int64_t) +
+                              (size_t)8 * maxsim_passes(plan) * sizeof(int32_t) <=
+                          sizeof(scratch)) {
+    sync = reinterpret_cast<int32_t*>(part + plan.n_ranges + 1);
+    n_sync = 8 * maxsim_passes(plan);
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = launch_partition(d_off, n_docs, n_tok, plan.n_ranges, part, nullptr, 0, s);
+  hipError_t e = launch_partition(d_off, n_docs, n_tok, plan.n_ranges, part, sync, n_sync, s);
   if (e != hipSuccess) return hip_fail(e, "partition launch");
-  e = launch_maxsim(plan, q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, part, scores, nullptr,
-                    nullptr, 0, s);
+  for (int pass = 0; pass < maxsim_passes(plan) && e == hipSuccess; ++pass)
+    e = launch_maxsim(plan, pass, q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, part, scores,
+                      nullptr, sync, n_sync, s);
   return e == hipSuccess ? HPR_OK : hip_fail(e, "maxsim launch");
 }
 
@@ -381,7 +407,7 @@ hpr_status maxsim_topk(const uint16_t* q, int32_t nq, int32_t lq, const uint16_t
   float* scores = c.take<float>((size_t)nq * n_docs * sizeof(float));
   int64_t* part = c.take<int64_t>(part_bytes(n_docs));
   st = run_maxsim(q, nq, lq, d_tok, d_off, n_docs, n_tok, dim, scores, nullptr, nullptr, 0, part,
-                  s);
+                  part_bytes(n_docs), s);
   if (st != HPR_OK) return st;
   hipError_t e = timed("topk", s, [&] {
     return launch_topk_rows(scores, nq, n_docs, n_docs, k, out_scores, out_idx, s);

@@ -22,6 +22,9 @@ struct MaxsimPlan {
   int qpw;         // queries per wave
   int n_qgroups;   // workgroups along the query axis
   int n_ranges;    // document ranges (workgroups along the document axis)
+  bool persist;    // score kernel: one range per XCD, one launch of one resident round per pass
+                   // of query groups
+  int64_t grid;    // workgroups per launch
 };
 
 // Returns false when the shape is outside the supported limits.
@@ -38,7 +41,10 @@ hipError_t launch_partition(const int64_t* off, int64_t n_docs, int64_t n_tok, i
 // launch_partition.  With amax it finds its ranges itself (part is not read), zeroes
 // ctrl[0 .. n_ctrl) (the control words of the later kernels of the call; ctrl may be null), and
 // scores a document longer than 65536 tokens as NaN.
-hipError_t launch_maxsim(const MaxsimPlan& plan, const uint16_t* q, int nq, int lq,
+// Launches per call of the score kernel (passes of a persistent plan; 1 otherwise); pass p
+// of launch_maxsim scores query groups [p G / 8, (p + 1) G / 8) of a persistent plan.
+int maxsim_passes(const MaxsimPlan& plan);
+hipError_t launch_maxsim(const MaxsimPlan& plan, int pass, const uint16_t* q, int nq, int lq,
                          const uint16_t* d_tok, const int64_t* off, int64_t n_docs,
                          int64_t n_tok, int dim, const int64_t* part, float* scores,
                          uint16_t* amax, int32_t* ctrl, int n_ctrl, hipStream_t stream);

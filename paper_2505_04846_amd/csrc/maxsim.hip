@@ -94,14 +94,27 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB))) void maxsim_kerne
   const int col = lane & 31;
   const int half = lane >> 5;
 
-  // block -> (document range, query group); all uniform, kept in scalar registers
-  const uint32_t total = (uint32_t)a.n_qgroups * (uint32_t)a.n_ranges;
-  const uint32_t lin = (uint32_t)xcd_linear(blockIdx.x, total);
-  const int rng = __builtin_amdgcn_readfirstlane((int)(lin / (uint32_t)a.n_qgroups));
-  const int qg = __builtin_amdgcn_readfirstlane((int)(lin - (uint32_t)rng * a.n_qgroups));
+  // block -> (document range, query group); all uniform, kept in scalar registers.  Persistent
+  // grid (one resident round per launch, one launch per pass of query groups): workgroup b runs
+  // on XCD b % 8 and takes range b % 8 (the XCD's eighth of the store) for query group
+  // qg_base + b / 8, so the workgroups of an XCD start together and read the same tiles at
+  // about the same time, once from beyond the XCD's L2.  Otherwise one (range, query group)
+  // per workgroup, the workgroups sharing a range placed on one XCD.
+  int rng, qg;
+  if (a.persist) {
+    rng = (int)(blockIdx.x % (uint32_t)a.n_ranges);
+    qg = a.qg_base + (int)(blockIdx.x / (uint32_t)a.n_ranges);
+  } else {
+    const uint32_t total = (uint32_t)a.n_qgroups * (uint32_t)a.n_ranges;
+    const uint32_t lin = (uint32_t)xcd_linear(blockIdx.x, total);
+    rng = (int)(lin / (uint32_t)a.n_qgroups);
+    qg = (int)(lin - (uint32_t)rng * a.n_qgroups);
+  }
+  rng = __builtin_amdgcn_readfirstlane(rng);
+  qg = __builtin_amdgcn_readfirstlane(qg);
   const int d_begin = __builtin_amdgcn_readfirstlane((int)part[rng]);
   const int d_end = __builtin_amdgcn_readfirstlane((int)part[rng + 1]);
-  if (d_begin >= d_end) return;  // uniform for the whole workgroup
+  if (d_begin >= d_end || qg >= a.n_qgroups) return;  // uniform for the whole workgroup
   const int qwg = qg * WPW * a.qpw;  // first query of the workgroup
   const int q0 = qwg + wave * a.qpw;
   const bool wave_active = q0 < a.nq;  // idle waves still load tiles and meet the barriers
@@ -309,6 +322,25 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB))) void maxsim_kerne
   bf16x8 fr[2];
   fr[0] = frag(0, 0, 0);
 
+  // Persistent plans keep the workgroups of a range in step: every kSyncStages stages each
+  // checks in on the range's counter (a.ctrl[8 pass + range], zeroed by the partition kernel
+  // of the call) and waits until all n_sync workgroups of the range have, for at most kMaxSpins
+  // sleeps; a workgroup whose wait runs out stops waiting for the rest of the launch (so a peer
+  // that is not resident costs one wait, and no wait can hang).  Correctness never depends on
+  // it: it only keeps the tiles of a range within reach of the XCD's L2.
+  constexpr int kSyncStages = 256, kMaxSpins = 4096;
+  int32_t* sync = nullptr;
+  int n_sync = 0;
+  __shared__ int sync_gave_up;  // written by thread 0 before the checkpoint's barrier
+  if (tid == 0) sync_gave_up = 0;
+  if (a.persist && a.n_ctrl > 0) {
+    const int per_pass = (int)(gridDim.x / (uint32_t)a.n_ranges);
+    const int pass = a.qg_base / per_pass;
+    if (8 * pass + rng < a.n_ctrl) {
+      sync = a.ctrl + 8 * pass + rng;
+      n_sync = a.n_qgroups - a.qg_base < per_pass ? a.n_qgroups - a.qg_base : per_pass;
+    }
+  }
   // Pipeline state (uniform): whether the tile whose epilogue runs next ends its document, and
   // where that document's result goes.  (The first tile's "previous tile" is acc = -inf, whose
   // epilogue changes nothing: one code path, whose registers fit without spills.)
@@ -335,6 +367,22 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB))) void maxsim_kerne
     if (more) store_stage(buf ^ 1);
     __syncthreads();
     if (!more) break;
+    if (sync && (stage & (kSyncStages - 1)) == kSyncStages - 1) {
+      // checkpoint: wait (bounded) until every workgroup of this range has reached it
+      if (tid == 0) {
+        const int target = (stage / kSyncStages + 1) * n_sync;
+        atomicAdd(sync, 1);
+        int spin = 0;
+        while (__hip_atomic_load(sync, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target &&
+               spin < kMaxSpins) {
+          __builtin_amdgcn_s_sleep(8);
+          ++spin;
+        }
+        sync_gave_up = spin == kMaxSpins ? 1 : 0;
+      }
+      __syncthreads();
+      if (sync_gave_up) sync = nullptr;  // a peer never came: stop waiting (workgroup-uniform)
+    }
     fr[0] = frag(buf ^ 1, 0, 0);
     prv2 = prv;
     prv = cur;
@@ -395,8 +443,7 @@ __global__ void fill_u64_kernel(unsigned long long* p, unsigned long long v) { *
 
 template <int KS, int NB, int WPW>
 hipError_t launch_t(const MaxsimPlan& plan, const MaxsimArgs& args, hipStream_t stream) {
-  const int64_t blocks = (int64_t)plan.n_qgroups * plan.n_ranges;
-  hipLaunchKernelGGL((maxsim_kernel<KS, NB, WPW>), dim3((unsigned)blocks), dim3(64 * WPW), 0,
+  hipLaunchKernelGGL((maxsim_kernel<KS, NB, WPW>), dim3((unsigned)plan.grid), dim3(64 * WPW), 0,
                      stream, args, args.off, args.part);
   return hipGetLastError();
 }
@@ -472,6 +519,21 @@ bool maxsim_plan(int nq, int lq, int64_t n_docs, int64_t n_tok, int dim, bool ar
   if (R < 1) R = 1;
   if ((int64_t)p->n_qgroups * R > 0x7fffffffLL) return false;
   p->n_ranges = (int)R;
+  // Persistent grid for the score kernel when the query groups fill every resident slot of an
+  // XCD at least twice, a whole number of times (or at least 8 times, the partial last pass
+  // then costing at most an eighth): one range per XCD, one launch of one resident round per
+  // pass.  (With a single pass the dynamically scheduled short ranges finish sooner: a long
+  // persistent range waits for its slowest workgroup.)
+  p->persist = false;
+  p->grid = (int64_t)p->n_qgroups * p->n_ranges;
+  if (!argmax && n_cu > 0 && n_cu % 8 == 0 && (int64_t)n_tok >= 8 * 1024 && n_docs >= 8) {
+    const int slots = n_cu / 8 * occ;  // resident workgroups per XCD
+    if (p->n_qgroups >= 2 * slots && (p->n_qgroups % slots == 0 || p->n_qgroups >= 8 * slots)) {
+      p->persist = true;
+      p->n_ranges = 8;
+      p->grid = (int64_t)8 * slots;
+    }
+  }
   return true;
 }
 
@@ -484,7 +546,13 @@ hipError_t launch_partition(const int64_t* off, int64_t n_docs, int64_t n_tok, i
   return hipGetLastError();
 }
 
-hipError_t launch_maxsim(const MaxsimPlan& plan, const uint16_t* q, int nq, int lq,
+int maxsim_passes(const MaxsimPlan& plan) {
+  if (!plan.persist) return 1;
+  const int64_t per_pass = plan.grid / plan.n_ranges;
+  return (int)((plan.n_qgroups + per_pass - 1) / per_pass);
+}
+
+hipError_t launch_maxsim(const MaxsimPlan& plan, int pass, const uint16_t* q, int nq, int lq,
                          const uint16_t* d_tok, const int64_t* off, int64_t n_docs,
                          int64_t n_tok, int dim, const int64_t* part, float* scores,
                          uint16_t* amax, int32_t* ctrl, int n_ctrl, hipStream_t stream) {
@@ -506,6 +574,8 @@ hipError_t launch_maxsim(const MaxsimPlan& plan, const uint16_t* q, int nq, int 
   args.dim = dim;
   args.n_qgroups = plan.n_qgroups;
   args.n_ranges = plan.n_ranges;
+  args.persist = plan.persist ? 1 : 0;
+  args.qg_base = plan.persist ? pass * (int)(plan.grid / plan.n_ranges) : 0;
   return launch_variant(plan, args, amax != nullptr, stream);
 }
 

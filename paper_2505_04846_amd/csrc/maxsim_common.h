@@ -22,6 +22,8 @@ struct MaxsimArgs {
   int32_t* ctrl;        // argmax kernel: control words of the call, zeroed by workgroup 0
   int64_t n_docs, n_tok;
   int nq, lq, lqp, qpw, dim, n_qgroups, n_ranges, n_ctrl;
+  int persist;          // score kernel: persistent grid (see maxsim_kernel) ...
+  int qg_base;          // ... and the first query group of the launch
 };
 
 // Position of tile `t` of the current document stream; uniform across the workgroup.  Token

@@ -133,6 +133,26 @@ def test_maxsim_many_ranges_and_query_groups():
     _assert_close(S, O, rel=1e-4, what="scores")
 
 
+def test_maxsim_persistent_passes_match_oracle():
+    # 1,024 queries of 64 tokens: 128 query groups of 8, two passes of the persistent grid (one
+    # document range per XCD, checkpoint counters after the range table); the result must not
+    # depend on the plan: the no-allocation entry point (its scratch holds the same table and
+    # counters) gives the same bits
+    g = torch.Generator().manual_seed(11)
+    lens = torch.randint(1, 90, (420,), generator=g)
+    Q, D, off = _ragged(12, 1024, 64, lens.tolist(), 128)
+    Qd, Dd, od = _to_dev(Q, D, off)
+    S = hpr.maxsim_score(Qd, Dd, od)
+    S2 = hpr.maxsim_score_noalloc(Qd, Dd, od)
+    assert torch.equal(S, S2)
+    O = oracle.maxsim_scores(_bf(Q), _bf(D), off.numpy())
+    _assert_close(S.cpu().numpy(), O, rel=1e-4, what="scores")
+    s, i = hpr.maxsim_topk(Qd, Dd, od, 40)
+    s, i = s.cpu().numpy(), i.cpu().numpy()
+    for q in (0, 7, 8, 511, 512, 1023):
+        check_topk(s[q], i[q], O[q], 40)
+
+
 def test_maxsim_document_token_order_is_bit_invariant():
     Q, D, off = _ragged(21, 6, 32, [70, 33, 128], 128)
     S1 = hpr.maxsim_score(*_to_dev(Q, D, off))
