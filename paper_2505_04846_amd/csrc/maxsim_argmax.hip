@@ -360,10 +360,11 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
       if (!((sd.valid >> j) & 1u)) break;
       if ((sd.last >> j) & 1u) {
         // a document too long for 16-bit argmax offsets scores NaN, which the loss carries on
+        // (stored as the bit pattern: this file is compiled assuming no NaN arithmetic)
         const bool lng = (sd.lng >> j) & 1u;
         if (tid < n_wg_q)
-          a.scores[(int64_t)(qwg + tid) * a.n_docs + d] =
-              lng ? __builtin_nanf("") : res_score[rb][j][tid];
+          reinterpret_cast<uint32_t*>(a.scores)[(int64_t)(qwg + tid) * a.n_docs + d] =
+              lng ? 0x7fc00000u : __float_as_uint(res_score[rb][j][tid]);
         uint16_t* dst = a.amax + (int64_t)d * n_entries + (int64_t)qwg * a.lq;
         for (int e = tid; e < n_wg_e; e += kThreads) dst[e] = res_amax[rb][j][e];
         ++d;
