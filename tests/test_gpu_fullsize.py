@@ -7,12 +7,14 @@ stores in full, so:
   * every query's list is checked for structure (indices in range and distinct, sorted by
     (score desc, index asc));
   * a seeded sample of returned (query, index, score) entries is checked against the oracle's
-    score of that (query, document), computed one by one (tolerance 2e-3 and the tight 1e-4 for
-    MaxSim, whose bf16 products are exact in fp32);
+    score of that (query, document), computed one by one (tolerance 2e-3, and again the tight
+    1e-4: bf16 and fp16 products are exact in fp32, so only the fp32 summation differs);
   * for a few queries the exact top-k set is checked against the oracle over a candidate set
     screened in float64 by plain torch (tests/screen.py), with the screening margin asserted, at
     the 2e-3 tolerance and again at a tight one (1e-5 for MaxSim, 1e-4 for the dense store);
-  * the dense store's 1,000 planted near-duplicates must each rank first for their query.
+  * the dense store's 1,000 planted near-duplicates must each rank first for their query;
+  * the sentence stream's decisions and segment ids over three windows of 30 whole papers must
+    be the oracle's (decisions within 2e-5 of the threshold excepted).
 """
 
 import numpy as np
@@ -140,15 +142,25 @@ def test_dense_retrieval_fullsize():
     pq, pr = w["planted_q"].cpu().numpy(), w["planted_row"].cpu().numpy()
     assert np.array_equal(i[pq, 0], pr), "a planted row is not its query's first result"
     Qh = _f16(Q)
-    o = np.sum(Qh[pq] * _f16(X[torch.as_tensor(pr, device=DEV)]), axis=1)
+
+    def oracle_pairs(qs, rows):
+        # the oracle's score of each (query, store row) pair, one pair at a time
+        Xr = _f16(X[torch.as_tensor(rows, device=DEV)])
+        return np.array([oracle.dense_scores(Qh[q][None], Xr[j][None])[0, 0]
+                         for j, q in enumerate(qs)])
+
+    o = oracle_pairs(pq, pr)
     assert np.all(np.abs(s[pq, 0] - o) <= REL * np.abs(o))
+    assert np.all(np.abs(s[pq, 0] - o) <= 1e-4 * np.abs(o))
     rng = np.random.default_rng(0)
     pick_q = rng.integers(0, nq, 300)
     pick_r = rng.integers(0, k, 300)
-    rows = torch.as_tensor(i[pick_q, pick_r], device=DEV)
-    want = np.sum(Qh[pick_q] * _f16(X[rows]), axis=1)
+    want = oracle_pairs(pick_q, i[pick_q, pick_r])
     got = s[pick_q, pick_r]
-    assert np.all(np.abs(got - want) <= REL * np.maximum(np.abs(want), 1e-3))
+    err = np.abs(got - want)
+    assert np.all(err <= REL * np.maximum(np.abs(want), 1e-3)), "sampled score outside 2e-3"
+    # fp16 products are exact in fp32, so only the fp32 summation of 4096 terms separates them
+    assert np.all(err <= 1e-4 * np.maximum(np.abs(want), 1e-3)), "sampled score outside 1e-4"
     unplanted = sorted(set(range(nq)) - set(pq.tolist()))
     for q in [int(pq[0]), int(pq[-1]), unplanted[0], unplanted[-1]]:
         row = dense_row_f64(Q[q], X)
@@ -168,8 +180,9 @@ def test_dense_retrieval_fullsize():
 
 def test_semantic_chunk_fullsize():
     # the benchmark's stream (10,000 papers, ~2M sentences of dim 4096) through the benchmark's
-    # call: every id is the prefix count of the GPU's own decisions, and sampled cosines (paper
-    # starts, their neighbours and random sentences) are checked against the oracle one by one
+    # call: every id is the prefix count of the GPU's own decisions, sampled cosines (paper
+    # starts, their neighbours and random sentences) are checked against the oracle one by one,
+    # and three windows of 30 whole papers are segmented by the oracle
     w = synth.sentence_stream(seed=0, device=DEV)
     E, off, thr = w["E"], w["paper_off"], w["threshold"]
     n = E.shape[0]
@@ -197,3 +210,21 @@ def test_semantic_chunk_fullsize():
         assert abs(cg[t] - o) <= 2e-5, (t, cg[t], o)
         if abs(o - thr) > 2e-5:
             assert bool(cg[t] > thr) == bool(o > thr), t
+    # whole papers at the start, middle and end of the stream through the oracle's steps 1-3:
+    # every decision away from the threshold, and the ids relative to the window's first
+    # sentence, must be the oracle's
+    seg = r["seg"].to(torch.int64).cpu().numpy()
+    n_papers = offh.size - 1
+    for p0 in [0, n_papers // 2 - 15, n_papers - 30]:
+        a, b = int(offh[p0]), int(offh[p0 + 30])
+        Eh = oracle.decode_fp16(E[a:b].cpu().view(torch.int16).numpy())
+        o_cos, o_seg, o_n = oracle.semantic_segments(Eh, offh[p0:p0 + 31] - a, thr)
+        near = np.abs(o_cos - thr) <= 2e-5
+        g_bnd = bnd[a:b].cpu().numpy()
+        o_bnd = np.r_[True, o_seg[1:] != o_seg[:-1]]
+        assert np.array_equal(g_bnd[~near], o_bnd[~near]), f"papers {p0}..{p0 + 29}: decisions"
+        if not near.any():
+            assert np.array_equal(seg[a:b] - seg[a], o_seg), f"papers {p0}..{p0 + 29}: ids"
+            assert int(g_bnd.sum()) == o_n
+        print(f"papers {p0}..{p0 + 29}: {b - a} sentences, {o_n} oracle segments, "
+              f"{int(near.sum())} near the threshold")
