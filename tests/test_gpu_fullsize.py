@@ -9,9 +9,10 @@ stores in full, so:
   * a seeded sample of returned (query, index, score) entries is checked against the oracle's
     score of that (query, document), computed one by one (tolerance 2e-3, and again the tight
     1e-4: bf16 and fp16 products are exact in fp32, so only the fp32 summation differs);
-  * for a few queries the exact top-k set is checked against the oracle over a candidate set
-    screened in float64 by plain torch (tests/screen.py), with the screening margin asserted, at
-    the 2e-3 tolerance and again at a tight one (1e-5 for MaxSim, 1e-4 for the dense store);
+  * for eight queries per store the exact top-k set is checked against the oracle over a
+    candidate set screened in float64 by plain torch (tests/screen.py), with the screening margin
+    asserted, at the 2e-3 tolerance and again at a tight one (1e-5 for MaxSim, 1e-4 for the dense
+    store);
   * the dense store's 1,000 planted near-duplicates must each rank first for their query;
   * the sentence stream's decisions and segment ids over three windows of 30 whole papers must
     be the oracle's (decisions within 2e-5 of the threshold excepted).
@@ -116,7 +117,8 @@ def _maxsim_fullsize(w, n_samples, queries, m_screen):
 def test_li_retrieval_fullsize():
     # 1,024 x 32 queries vs 500,000 documents (Ld uniform in [32, 384]), dim 128, top-100
     w = synth.li_retrieval(seed=0, device=DEV)
-    _maxsim_fullsize(w, n_samples=400, queries=[0, 1, 517, 1023], m_screen=1000)
+    _maxsim_fullsize(w, n_samples=400, queries=[0, 1, 100, 333, 517, 768, 900, 1023],
+                     m_screen=1000)
     del w
     torch.cuda.empty_cache()
 
@@ -124,7 +126,8 @@ def test_li_retrieval_fullsize():
 def test_li_large_fullsize():
     # 4,096 x 64 queries vs 1,000,000 lognormal documents with 10 % noisy clones, top-1000
     w = synth.li_large(seed=0, device=DEV)
-    _maxsim_fullsize(w, n_samples=300, queries=[0, 2049, 4095], m_screen=3000)
+    _maxsim_fullsize(w, n_samples=300, queries=[0, 1, 777, 1500, 2049, 3000, 3333, 4095],
+                     m_screen=3000)
     del w
     torch.cuda.empty_cache()
 
@@ -162,7 +165,8 @@ def test_dense_retrieval_fullsize():
     # fp16 products are exact in fp32, so only the fp32 summation of 4096 terms separates them
     assert np.all(err <= 1e-4 * np.maximum(np.abs(want), 1e-3)), "sampled score outside 1e-4"
     unplanted = sorted(set(range(nq)) - set(pq.tolist()))
-    for q in [int(pq[0]), int(pq[-1]), unplanted[0], unplanted[-1]]:
+    for q in [int(pq[0]), int(pq[1]), int(pq[500]), int(pq[-1]), unplanted[0], unplanted[1000],
+              unplanted[2000], unplanted[-1]]:
         row = dense_row_f64(Q[q], X)
         cand, outside = candidates(row, i[q], 1000)
         del row
