@@ -302,7 +302,7 @@ def build_workload(name, dev, scale, tau, nq_sub=None):
         return dict(step=step, pairs=nq, kernel="dense_scan", flops=flops, bytes=sbytes, after=after,
                     metric="top-k queries/sec + % fp16 MFMA peak",
                     cpu_sample=cpu_sample, config=cfg, dtype="fp16", unit="queries/s",
-                    sha=source_sha("dense.hip", "common.h"))
+                    sha=source_sha("dense.hip", "common.h", "kernels.h"))
 
     if name == "semantic_chunk":
         w = synth.sentence_stream(seed=0, device=dev)
