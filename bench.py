@@ -343,7 +343,7 @@ def build_workload(name, dev, scale, tau, nq_sub=None):
                     config=cfg, dtype="fp16", unit="sentences/s",
                     sha=source_sha("chunking.hip", "common.h"))
 
-    raise SystemExit(f"workload {name} is not available in this build")
+    raise SystemExit(f"unknown workload {name}")
 
 
 def cpu_subset(args):
@@ -438,9 +438,8 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(the sharding design is described in DESIGN.md); run with --gpus 1",
-              file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path; "
+              "run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     if args.cpu_subset:

@@ -61,14 +61,14 @@ typedef int32_t hpr_status;
 #define HPR_ERR_INVALID_ARG 1         /* NULL pointer, non-positive size, k out of range ...   */
 #define HPR_ERR_BAD_CSR 2             /* hpr_csr_validate: offsets not a valid CSR             */
 #define HPR_ERR_EMPTY_DOC 3           /* hpr_csr_validate: a document with no token            */
-#define HPR_ERR_UNSUPPORTED_SHAPE 4   /* valid, but outside the limits this build supports     */
+#define HPR_ERR_UNSUPPORTED_SHAPE 4   /* valid, but outside the limits this version supports   */
 #define HPR_ERR_WORKSPACE_TOO_SMALL 5 /* ws_bytes below the *_workspace_size() value            */
 #define HPR_ERR_CAPACITY 6            /* reserved: no entry point of this version returns it    */
 #define HPR_ERR_HIP 7                 /* a HIP runtime call or kernel launch failed             */
 
 #define HPR_ABI_VERSION 1
 
-/* Shape limits of this build (HPR_ERR_UNSUPPORTED_SHAPE beyond them).
+/* Shape limits of this version (HPR_ERR_UNSUPPORTED_SHAPE beyond them).
  *   MaxSim calls: dim % 8 == 0, 8 <= dim <= 256; lq <= 128 when dim <= 128, lq <= 64 when
  *     dim <= 256; coltrast_loss_fwd_bwd: lq <= 64 when dim <= 128, lq <= 32 when dim <= 256;
  *     n_tok < 2^31 (a store of 2^31 bf16 tokens of dim 128 would not fit one GPU's HBM).

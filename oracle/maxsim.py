@@ -62,7 +62,7 @@ def maxsim_argmax(Q, D, offsets):
 
     Returns (S, A): S as in `maxsim_scores`; A int64 [nq, lq, n_docs] with A[q, i, d] = the
     LOWEST local token index j (0 <= j < Ld) attaining max_j <Q[q, i], D[off[d] + j]>.  The
-    lowest index is this build's reading for ties (the paper does not discuss them); it decides
+    lowest index is the reading taken here for ties (the paper does not discuss them); it decides
     which document token receives the subgradient of the max.
     """
     Q = np.asarray(Q, dtype=np.float64)

@@ -75,7 +75,7 @@ hpr_status scratch_address(int64_t** out) {
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   if (dev < 0 || dev >= kMaxDevices)
-    return fail(HPR_ERR_UNSUPPORTED_SHAPE, "device %d beyond the %d this build tracks", dev,
+    return fail(HPR_ERR_UNSUPPORTED_SHAPE, "device %d beyond the %d devices the library tracks", dev,
                 kMaxDevices);
   std::lock_guard<std::mutex> g(g_scratch_mu);
   if (!g_scratch_ptr[dev]) {

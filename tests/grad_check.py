@@ -1,4 +1,4 @@
-"""Per-row checker for the loss gradients dQ and dD against the oracle's.
+"""Per-row verification of the loss gradients dQ and dD against the oracle's.
 
 The gradient of the MaxSim score reaches one document token per (query token, document): the
 token attaining the maximum (lowest index on ties).  The GPU decides that maximum on fp32 dot
@@ -6,7 +6,7 @@ products (and on argmax keys that drop the 4 low mantissa bits), the oracle on f
 two tokens of a document come within 1e-5 of each other for a query token (a "near-tie"), both
 choices are valid and the subgradient may legitimately go to either.  Such a choice moves
 G[q, d] * Q[q, i] from one dD row to another and changes the dQ row of (q, i) by
-G[q, d] * (D[j'] - D[j]).  Rather than excusing whole rows, the checker widens each row's bound
+G[q, d] * (D[j'] - D[j]).  Rather than excusing whole rows, the verification widens each row's bound
 by exactly what those alternative choices can move:
 
   allow_dQ[q, i] = sum over near-ties (q, i, d) of |G[q, d]| * max_{j' in window} |D[j'] - D[j]|

@@ -65,7 +65,7 @@ def candidates(screen_row, gpu_idx, m):
 def virtual_row(n, cand, oracle_scores, floor):
     """An n-entry oracle row holding the oracle's scores at `cand` and `floor` elsewhere (every
     non-candidate is proven to lie below the k-th score minus the tolerance, and `floor` is below
-    all of them), for the top-k checker."""
+    all of them), for the top-k rules of tests/topk_check.py."""
     row = np.full(n, floor, dtype=np.float64)
     row[cand] = oracle_scores
     return row

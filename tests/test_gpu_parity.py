@@ -1,7 +1,7 @@
 """GPU parity: every entry point of the HIP library against the fp64 oracle on seeded inputs.
 
-Tolerances (scores and loss): |gpu - oracle| <= 2e-3 * max(|oracle|, 1e-3), the bound the task
-sets for bf16 inputs with fp32 accumulation; a 20x tighter check (1e-4) is also asserted on
+Tolerances (scores and loss): |gpu - oracle| <= 2e-3 * max(|oracle|, 1e-3), the stated bound
+for bf16 inputs with fp32 accumulation; a 20x tighter check (1e-4) is also asserted on
 MaxSim scores because bf16 x bf16 products are exact in fp32 and only the fp32 summation differs
 from the oracle.  Gradients: relative L2 error <= 2e-3 per tensor and per row (tests/grad_check.py:
 a row's bound widens only by what argmax near-ties may legitimately move).  Top-k lists: the rules of

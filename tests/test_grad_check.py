@@ -1,4 +1,4 @@
-"""CPU checks of the per-row gradient checker (tests/grad_check.py): it must accept the oracle's
+"""CPU checks of the per-row gradient verification (tests/grad_check.py): it must accept the oracle's
 own gradients and the alternative a near-tie allows, and reject planted mistakes (a scaled
 row in a document of small softmax weight, a dropped row, a row moved without a tie)."""
 

@@ -1,8 +1,8 @@
-"""Checker for a GPU top-k list against oracle scores of every candidate.
+"""Verification of a GPU top-k list against oracle scores of every candidate.
 
 With floating-point scores several answers can be right: the GPU computes scores in fp32 from
 bf16/fp16 products, the oracle in fp64, and documents whose scores lie within the tolerance of
-the k-th score may legitimately swap places.  The checker therefore verifies what is unique
+the k-th score may legitimately swap places.  This module therefore verifies what is unique
 and that the rest is valid, at tolerance T(x) = rel * max(|x|, 1e-3):
 
   1. indices are distinct and in range; the list is sorted by (GPU score desc, index asc);
