@@ -18,7 +18,7 @@ import torch
 import oracle
 import paper_2505_04846_amd as hpr
 import synth
-from grad_check import check_rows, near_tie_allowance
+from grad_check import check_rows, conditioning_allowance, near_tie_allowance
 from topk_check import check_topk
 
 pytestmark = pytest.mark.gpu
@@ -295,8 +295,10 @@ def _loss_parity(Q, D, off, pos, scale, rel_grad=REL, max_allowed=0.5):
     assert e_dd <= rel_grad, f"dD rel L2 {e_dd:.3g}"
     # every row on its own: rel L2 2e-3, widened only by what argmax near-ties may move
     aq, ad, _ = near_tie_allowance(Qo, Do, off.numpy(), o["G"])
-    fq = check_rows(dq, o["dQ"], aq, "dQ rows", rel_grad)
-    fd = check_rows(dd, o["dD"], ad, "dD rows", rel_grad)
+    cq, cd = conditioning_allowance(Qo, Do, off.numpy(), o["G"], o["A"],
+                                    r["scores"].cpu().numpy() - o["S"], scale)
+    fq = check_rows(dq, o["dQ"], aq, "dQ rows", rel_grad, cond=cq)
+    fd = check_rows(dd, o["dD"], ad, "dD rows", rel_grad, cond=cd)
     assert fq <= max_allowed and fd <= max_allowed, (fq, fd)
     return r, o
 
