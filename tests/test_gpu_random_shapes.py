@@ -79,14 +79,15 @@ def test_maxsim_score_random_shapes():
 
 def test_maxsim_topk_random_shapes():
     rng = np.random.default_rng(202)
-    for c in range(8):
-        dim = _dim(rng, 128)
+    for c in range(10):
+        long_rows = c >= 8  # rows long enough for the streaming select
+        dim = _dim(rng, 32 if long_rows else 128)
         lq = int(rng.integers(1, 33))
         nq = int(rng.integers(1, 9))
-        n_docs = int(rng.integers(1, 3001))
+        n_docs = int(rng.integers(9_000, 40_001)) if long_rows else int(rng.integers(1, 3001))
         k = int(rng.integers(1, min(n_docs, 1024) + 1))
         print(f"config {c}: nq={nq} lq={lq} dim={dim} n_docs={n_docs} k={k}", flush=True)
-        Q, D, off = _store(rng, nq, lq, dim, n_docs, 24, plant=True)
+        Q, D, off = _store(rng, nq, lq, dim, n_docs, 4 if long_rows else 24, plant=True)
         s, i = hpr.maxsim_topk(Q.to(DEV), D.to(DEV), off.to(DEV), k)
         s, i = s.cpu().numpy(), i.cpu().numpy()
         O = oracle.maxsim_scores(oracle.decode_bf16(_bits(Q)), oracle.decode_bf16(_bits(D)),
@@ -119,6 +120,36 @@ def test_loss_random_shapes():
         # copies of a query's token in its positive and in a negative make rows whose terms
         # cancel: their bound includes what fp32 weights and sums cannot resolve
         cq, cd = conditioning_allowance(Qo, Do, off.numpy(), o["G"], o["A"], S - o["S"], scale)
+        check_rows(r["dq"].cpu().numpy(), o["dQ"], aq, f"config {c} dQ", cond=cq)
+        check_rows(r["dd"].cpu().numpy(), o["dD"], ad, f"config {c} dD", cond=cd)
+
+
+def test_total_loss_random_shapes():
+    rng = np.random.default_rng(606)
+    for c in range(8):
+        dim = _dim(rng, 256)
+        lq = int(rng.integers(1, (64 if dim <= 128 else 32) + 1))
+        nq = int(rng.integers(1, 17))
+        n_docs = int(rng.integers(1, 41))
+        scale = float(np.exp(rng.uniform(np.log(0.3), np.log(30.0))))
+        tau = float(np.exp(rng.uniform(np.log(0.02), np.log(1.0))))
+        print(f"config {c}: nq={nq} lq={lq} dim={dim} n_docs={n_docs} scale={scale:.3f} "
+              f"tau={tau:.3f}", flush=True)
+        Q, D, off = _store(rng, nq, lq, dim, n_docs, 200, plant=True)
+        pos = torch.as_tensor(rng.integers(0, n_docs, nq), dtype=torch.int32)
+        args = (Q.to(DEV), D.to(DEV), off.to(DEV), pos.to(DEV), scale)
+        r = hpr.coltrast_total_loss_fwd_bwd(*args, tau)
+        S = hpr.coltrast_loss_fwd_bwd(*args, return_scores=True)["scores"].cpu().numpy()
+        Qo, Do = oracle.decode_bf16(_bits(Q)), oracle.decode_bf16(_bits(D))
+        o = oracle.coltrast_total_loss(Qo, Do, off.numpy(), pos.numpy(), scale, tau)
+        li = oracle.coltrast_li_loss(Qo, Do, off.numpy(), pos.numpy(), scale)
+        got = r["loss"].cpu().numpy()
+        for j, key in enumerate(("loss", "loss_li", "loss_c")):
+            _close(got[j], o[key], REL, f"config {c} {key}")
+        # the L_LI half carries weights G / 2
+        aq, ad, _ = near_tie_allowance(Qo, Do, off.numpy(), 0.5 * li["G"])
+        cq, cd = conditioning_allowance(Qo, Do, off.numpy(), 0.5 * li["G"], li["A"], S - li["S"],
+                                        scale)
         check_rows(r["dq"].cpu().numpy(), o["dQ"], aq, f"config {c} dQ", cond=cq)
         check_rows(r["dd"].cpu().numpy(), o["dD"], ad, f"config {c} dD", cond=cd)
 
