@@ -71,10 +71,14 @@ def test_maxsim_score_random_shapes():
               flush=True)
         Q, D, off = _store(rng, nq, lq, dim, n_docs, max_len, plant=c % 2 == 0)
         S = hpr.maxsim_score(Q.to(DEV), D.to(DEV), off.to(DEV)).cpu().numpy()
-        O = oracle.maxsim_scores(oracle.decode_bf16(_bits(Q)), oracle.decode_bf16(_bits(D)),
-                                 off.numpy())
+        Qo, Do = oracle.decode_bf16(_bits(Q)), oracle.decode_bf16(_bits(D))
+        O, A = oracle.maxsim_argmax(Qo, Do, off.numpy())
         _close(S, O, REL, f"config {c}")
-        _close(S, O, 1e-4, f"config {c} (tight)")
+        # the tight 1e-4 where the score is not a near-cancellation of its per-token maxima
+        # (single-token documents can sum maxima of both signs to ~0, below fp32 resolution)
+        m = np.abs(np.einsum("qik,qidk->qid", Qo, Do[off.numpy()[:-1][None, None, :] + A]))
+        well = m.sum(axis=1) <= 10.0 * np.maximum(np.abs(O), 1e-3)
+        _close(S[well], O[well], 1e-4, f"config {c} (tight)")
 
 
 def test_maxsim_topk_random_shapes():
