@@ -101,10 +101,10 @@ def traffic(args):
 
 
 def _agent(d):
-    """(XCD count, SIMD count) of the GPU agent of a rocprofv3 run."""
+    """(XCD count, SIMD count, CU count) of the GPU agent of a rocprofv3 run."""
     for r in _csv(d, "*agent_info.csv"):
         if r.get("Agent_Type", "").upper().endswith("GPU") or r.get("Name", "").startswith("gfx"):
-            return int(r["Num_Xcc"]), int(r["Simd_Count"])
+            return int(r["Num_Xcc"]), int(r["Simd_Count"]), int(r["Cu_Count"])
     raise SystemExit(f"no GPU agent in {d}")
 
 
@@ -113,9 +113,9 @@ def counters(args):
     more `rocprofv3 --pmc` runs (each run's counters are averaged over its matching dispatches;
     every run must have collected GRBM_GUI_ACTIVE, which sums the busy cycles of all XCDs)."""
     merged, durs = {}, []
-    n_xcc = n_simd = None
+    n_xcc = n_simd = n_cu = None
     for d in args.dirs:
-        n_xcc, n_simd = _agent(d)
+        n_xcc, n_simd, n_cu = _agent(d)
         rows = [r for r in _csv(d, "*counter_collection.csv") if args.match in r["Kernel_Name"]]
         if not rows:
             raise SystemExit(f"no dispatch of {args.match} in {d}")
@@ -139,7 +139,10 @@ def counters(args):
               f"{n_xcc} and {n_simd}):", ""]
     cyc = c.get("GRBM_GUI_ACTIVE", 0.0) / n_xcc  # busy cycles of one XCD
     if cyc:
-        lines.append(f"- clock: GRBM_GUI_ACTIVE / {n_xcc} / duration = {cyc / dur / 1e9:.3f} GHz")
+        ghz = cyc / dur / 1e9
+        note = (" (above the 2.4 GHz peak: for a dispatch this short the counter also holds cycles "
+                "outside it, so no clock is derived)" if ghz > 2.4 else "")
+        lines.append(f"- clock: GRBM_GUI_ACTIVE / {n_xcc} / duration = {ghz:.3f} GHz{note}")
     if cyc and "SQ_VALU_MFMA_BUSY_CYCLES" in c:
         lines.append(f"- MFMA busy: SQ_VALU_MFMA_BUSY_CYCLES / (cycles x {n_simd} SIMDs) = "
                      f"{c['SQ_VALU_MFMA_BUSY_CYCLES'] / (cyc * n_simd):.3f}")
@@ -153,6 +156,20 @@ def counters(args):
             lines.append(f"- other VALU instructions per MFMA: {(c['SQ_INSTS_VALU'] - m) / m:.2f}")
         if "SQ_INSTS_LDS" in c:
             lines.append(f"- LDS instructions per MFMA: {c['SQ_INSTS_LDS'] / m:.3f}")
+    if c.get("SQ_WAVE_CYCLES"):
+        w = c["SQ_WAVE_CYCLES"]
+        if "SQ_WAIT_ANY" in c:
+            lines.append(f"- waves waiting: SQ_WAIT_ANY / SQ_WAVE_CYCLES = {c['SQ_WAIT_ANY'] / w:.3f}")
+        if "SQ_ACTIVE_INST_ANY" in c:
+            lines.append(f"- waves issuing: SQ_ACTIVE_INST_ANY / SQ_WAVE_CYCLES = "
+                         f"{c['SQ_ACTIVE_INST_ANY'] / w:.3f}")
+    if "TA_TA_BUSY_sum" in c:
+        # GRBM_GUI_ACTIVE over-counts short dispatches under the profiler, so the busy cycles
+        # are also set against the dispatch's duration at the 2.4 GHz peak clock (a lower bound
+        # on the busy fraction at any lower clock)
+        per_cu = c["TA_TA_BUSY_sum"] / n_cu
+        lines.append(f"- texture-address units: {per_cu:.4g} busy cycles per CU; over the "
+                     f"dispatch's duration at 2.4 GHz: {per_cu / (dur * 2.4e9):.3f}")
     if "TCC_HIT_sum" in c and "TCC_MISS_sum" in c:
         h, mi = c["TCC_HIT_sum"], c["TCC_MISS_sum"]
         lines.append(f"- L2 hit rate: {h / (h + mi):.3f} ({mi:.4g} misses)")
