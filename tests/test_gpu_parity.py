@@ -334,6 +334,17 @@ def test_loss_small_shapes(nq, lq, lens, dim, scale):
     _loss_parity(Q, D, off, pos, scale)
 
 
+def test_loss_over_thousands_of_short_documents():
+    # 40 queries x 4,000 documents of 1-6 tokens: InfoNCE rows of 4,000 scores, argmax ranges
+    # of hundreds of documents, dD over many tiny documents
+    nq, lq = 40, 8
+    g = torch.Generator().manual_seed(41)
+    lens = torch.randint(1, 7, (4000,), generator=g).tolist()
+    Q, D, off = _ragged(41, nq, lq, lens, 64)
+    pos = torch.randint(0, len(lens), (nq,), generator=g, dtype=torch.int32)
+    _loss_parity(Q, D, off, pos, 2.0)
+
+
 @pytest.mark.parametrize("nq,lq", [(200, 32), (470, 32)])
 def test_loss_many_query_tokens(nq, lq):
     # 6,400 and 15,040 (query, token) entries: the dD kernel's LDS no longer fits two 512-thread
