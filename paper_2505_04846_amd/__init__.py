@@ -18,7 +18,10 @@ fallback: if the library is not built, or a call fails, an exception is raised.
     csr_validate(off, n_tok)                      -> (status name, first bad document or -1)
 
 Q and D are bf16 CUDA tensors ([nq, lq, dim] and [n_tok, dim]); off is int64 [n_docs + 1];
-pos is int32 [nq]; Q and X of dense_ip_topk are fp16 [nq, dim] and [n, dim].
+pos is int32 [nq]; Q and X of dense_ip_topk are fp16 [nq, dim] and [n, dim].  A valid CSR is a
+precondition of the MaxSim calls (the library never reads the offsets on the host); with the
+environment variable HPR_VALIDATE=1 every MaxSim call first checks it with csr_validate (one
+synchronisation) and raises HprError on an invalid one.
 """
 
 import ctypes
@@ -143,6 +146,11 @@ def _maxsim_inputs(Q, D, off):
     nq, lq, dim = Q.shape
     if D.shape[1] != dim:
         raise ValueError(f"D has dim {D.shape[1]}, Q has {dim}")
+    if os.environ.get("HPR_VALIDATE") == "1":  # debugging aid: checks the CSR, synchronising
+        status, doc = csr_validate(off, D.shape[0])
+        if status != "HPR_OK":
+            raise HprError({v: k for k, v in STATUS_NAMES.items()}[status],
+                           f"invalid CSR offsets (first bad document {doc})")
     return dev, nq, lq, dim, off.numel() - 1, D.shape[0]
 
 

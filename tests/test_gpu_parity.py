@@ -533,6 +533,18 @@ def test_concurrent_calls_on_two_streams_with_separate_workspaces():
             assert torch.equal(lb[key], ref_l[key]), key
 
 
+def test_validate_env_rejects_a_bad_csr_before_the_call(monkeypatch):
+    Q, D, off = _ragged(5, 2, 4, [3, 5, 2], 16)
+    bad = off.clone()
+    bad[2] = bad[1]  # an empty document
+    monkeypatch.setenv("HPR_VALIDATE", "1")
+    with pytest.raises(hpr.HprError) as e:
+        hpr.maxsim_score(*_to_dev(Q, D, bad))
+    assert e.value.status_name == "HPR_ERR_EMPTY_DOC"
+    S = hpr.maxsim_score(*_to_dev(Q, D, off)).cpu().numpy()  # a valid CSR passes
+    _assert_close(S, oracle.maxsim_scores(_bf(Q), _bf(D), off.numpy()), what="scores")
+
+
 def test_csr_validate():
     good = torch.tensor([0, 3, 4, 9], dtype=torch.int64, device=DEV)
     assert hpr.csr_validate(good, 9) == ("HPR_OK", -1)
