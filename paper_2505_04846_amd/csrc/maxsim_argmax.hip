@@ -15,6 +15,13 @@
 // epilogues (the last tile of a stage finishes in the next stage), and to HBM two stages later,
 // after a barrier has passed behind every epilogue of the stage: a ring of three result buffers.
 //
+// Staging.  At dim 128 the tiles go straight from global memory into LDS (buffer loads with
+// the LDS as destination), four tiles per stage, wave w loading tile w: the loads of stage s + 1
+// are issued when stage s starts, into the buffer stage s - 1 used, and each wave waits for its
+// own before the stage's closing barrier.  Against staging through VGPRs (two tiles per stage,
+// the registers the wider stage would need are not there) this halves the barriers and the
+// per-stage bookkeeping per tile and drops the LDS stores.  The other dims keep the VGPR path.
+//
 // Everything else (query operands in VGPRs, the document tile stream, the C layout, the K
 // permutation, XCD placement) is as in maxsim_kernel (maxsim.hip).
 #include <type_traits>
@@ -26,13 +33,20 @@ namespace msim {
 
 namespace {
 
-template <int KS>
+// DIRECT: the tiles are staged by direct-to-LDS buffer loads (only when dim = 16 KS, so that
+// every chunk of a row is data), one tile per wave and four per stage.  A wave load writes 1 KiB
+// of consecutive LDS bytes, 16 per lane, so a tile's region is rounded up to whole loads; the
+// lane that lands on a row's padding or past the tile's 32 rows loads row 0 of the tile into
+// bytes nobody reads.
+template <int KS, bool DIRECT>
 struct ArgGeom {
   static constexpr int kCpr = KS * 2;                  // 16-byte chunks per row
   static constexpr int kRowB = KS * 32 + 16;           // padded row
   static constexpr int kTileB = 32 * kRowB;
-  static constexpr int kTps = argmax_tps(KS);          // tiles per stage (even)
-  static constexpr int kStageB = kTps * kTileB;
+  static constexpr int kLoads = (kTileB + 1023) / 1024;  // direct loads per tile
+  static constexpr int kTileS = DIRECT ? kLoads * 1024 : kTileB;  // tile stride in a stage
+  static constexpr int kTps = DIRECT ? 4 : argmax_tps(KS);        // tiles per stage (even)
+  static constexpr int kStageB = kTps * kTileS;
 };
 
 // What the epilogue of a computed tile needs: its tile index within the document, whether it
@@ -80,10 +94,15 @@ __device__ int range_first_doc(const int64_t* __restrict__ off, int64_t n_docs, 
   return (int)lo;
 }
 
-template <int KS, int NB, int WPW>
+template <int KS, int NB, int WPW, bool DIRECT>
 __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
     MaxsimArgs a, const int64_t* __restrict__ off) {
-  using G = ArgGeom<KS>;
+  using G = ArgGeom<KS, DIRECT>;
+  static_assert(!DIRECT || G::kTps == WPW, "direct staging: one tile per wave");
+  // two workgroups per CU (what the plan assumes for every variant): two stages and the ring
+  static_assert(2 * (2 * G::kStageB + 3 * G::kTps * (WPW * NB * 4 + WPW * NB * 32 * 2)) <=
+                    160 * 1024,
+                "LDS of two resident workgroups");
   constexpr int kThreads = 64 * WPW;
   constexpr int kSlotsWG = WPW * NB * 32;
   constexpr int kTps = G::kTps;
@@ -163,7 +182,7 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
   constexpr int kUpt = kTps * kPpt / kTpp;
   TileCursor prod;
   open_doc(prod, d_begin);
-  u32x4 stage_regs[kUpt];
+  u32x4 stage_regs[DIRECT ? 1 : kUpt];
   const int lr = (tid / G::kCpr) & 31;
   const int lt = __builtin_amdgcn_readfirstlane((tid / G::kCpr) >> 5);
   const int lc = tid % G::kCpr;
@@ -175,17 +194,59 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
     __syncthreads();
   }
   const uint32_t row_bytes = 2u * (uint32_t)a.dim;
-  auto fetch_stage = [&](StageDesc& sd) {
+  // direct staging: this lane's source offset within the tile for each of the tile's loads
+  // (rows below 32 of the tile's first token; 0 for the lanes that fill padding)
+  auto direct_off = [&](int q, uint32_t rmx) {
+    const int p = q * 1024 + 16 * lane;
+    const int row = p / G::kRowB;
+    const int c = (p - row * G::kRowB) >> 4;
+    const uint32_t r = (uint32_t)row < rmx ? (uint32_t)row : rmx;
+    return (row < 32 && c < G::kCpr) ? r * (uint32_t)(32 * KS) + 16u * (uint32_t)c : 0u;
+  };
+  uint32_t doff[DIRECT ? G::kLoads : 1];
+  if constexpr (DIRECT) {
+#pragma unroll
+    for (int q = 0; q < G::kLoads; ++q) doff[q] = direct_off(q, 31u);
+  }
+  // direct staging: wave w loads tile w of the stage, whose first token is r0 and last row rmx
+  auto issue_tile = [&](int buf, int r0, uint32_t rmx) {
+    const char* tptr = reinterpret_cast<const char*>(a.d) + (uint64_t)(uint32_t)r0 * row_bytes;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char*>(tptr), (short)0, 0x7fffffff, 0x00020000);
+    unsigned char* dst = &lds[buf][wave * G::kTileS];
+    if (rmx >= 31u) {
+#pragma unroll
+      for (int q = 0; q < G::kLoads; ++q)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)(dst + 1024 * q), 16,
+                                                 (int)doff[q], 0, 0, 0);
+    } else {  // a document's last, partial tile: rows past its end repeat its last token
+#pragma unroll
+      for (int q = 0; q < G::kLoads; ++q)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)(dst + 1024 * q), 16,
+                                                 (int)direct_off(q, rmx), 0, 0, 0);
+    }
+  };
+  auto fetch_stage = [&](StageDesc& sd, int buf) {
     sd.d0 = prod.d;
     sd.t0 = prod.t;
     sd.valid = sd.last = sd.lng = 0u;
+    bool my_ok = false;
+    int my_r0 = 0;
+    uint32_t my_rmx = 0u;
 #pragma unroll
     for (int j = 0; j < kTps; ++j) {
       const bool ok = prod.d < d_end;
       const int r0 = ok ? prod.base + prod.t * 32 : 0;
       const uint32_t rmx = ok ? prod.len - prod.t * 32 - 1 : 0;
-      const char* tptr = reinterpret_cast<const char*>(a.d) + (uint64_t)(uint32_t)r0 * row_bytes;
-      if (j % kTpp == lt && lok) {
+      if constexpr (DIRECT) {
+        if (j == wave) {  // uniform
+          my_ok = ok;
+          my_r0 = r0;
+          my_rmx = rmx;
+        }
+      } else if (j % kTpp == lt && lok) {
+        const char* tptr =
+            reinterpret_cast<const char*>(a.d) + (uint64_t)(uint32_t)r0 * row_bytes;
 #pragma unroll
         for (int p = 0; p < kPpt; ++p) {
           const uint32_t row = lr + kRp * p;
@@ -205,6 +266,8 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
         }
       }
     }
+    if constexpr (DIRECT)
+      if (my_ok) issue_tile(buf, my_r0, my_rmx);
   };
   auto store_stage = [&](int buf) {
     if (!lok) return;
@@ -212,7 +275,7 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
     for (int m = 0; m < kUpt; ++m) {
       const int j = (m / kPpt) * kTpp + lt;
       const uint32_t row = lr + kRp * (m % kPpt);
-      *reinterpret_cast<u32x4*>(&lds[buf][j * G::kTileB + row * G::kRowB + lboff]) = stage_regs[m];
+      *reinterpret_cast<u32x4*>(&lds[buf][j * G::kTileS + row * G::kRowB + lboff]) = stage_regs[m];
     }
   };
 
@@ -235,7 +298,7 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
 
   // A operand fragment of k-step s of tile j in stage buffer `buf` (immediate offset 32 s).
   auto frag = [&](int buf, int j, int s) {
-    return as_bf16x8(*reinterpret_cast<const u32x4*>(&lds[buf][j * G::kTileB] + a_lane + 32 * s));
+    return as_bf16x8(*reinterpret_cast<const u32x4*>(&lds[buf][j * G::kTileS] + a_lane + 32 * s));
   };
   // The tile is processed in kRegions scheduling regions of kRs k-steps each (at most 4, so
   // that only two sets of A fragments are live); region p of the epilogue covers registers
@@ -353,32 +416,30 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
     }
   };
 
+  // the documents that end in a stage are consecutive from its first one, one per bit of `last`
   auto write_results = [&](const StageDesc& sd, int rb) {
     int d = sd.d0;
 #pragma unroll 1
-    for (int j = 0; j < kTps; ++j) {
-      if (!((sd.valid >> j) & 1u)) break;
-      if ((sd.last >> j) & 1u) {
-        // a document too long for 16-bit argmax offsets scores NaN, which the loss carries on
-        // (stored as the bit pattern: this file is compiled assuming no NaN arithmetic)
-        const bool lng = (sd.lng >> j) & 1u;
-        if (tid < n_wg_q)
-          reinterpret_cast<uint32_t*>(a.scores)[(int64_t)(qwg + tid) * a.n_docs + d] =
-              lng ? 0x7fc00000u : __float_as_uint(res_score[rb][j][tid]);
-        uint16_t* dst = a.amax + (int64_t)d * n_entries + (int64_t)qwg * a.lq;
-        for (int e = tid; e < n_wg_e; e += kThreads) dst[e] = res_amax[rb][j][e];
-        ++d;
-      }
+    for (uint32_t m = sd.last & sd.valid; m != 0u; m &= m - 1u, ++d) {
+      const int j = __builtin_ctz(m);
+      // a document too long for 16-bit argmax offsets scores NaN, which the loss carries on
+      // (stored as the bit pattern: this file is compiled assuming no NaN arithmetic)
+      const bool lng = (sd.lng >> j) & 1u;
+      if (tid < n_wg_q)
+        reinterpret_cast<uint32_t*>(a.scores)[(int64_t)(qwg + tid) * a.n_docs + d] =
+            lng ? 0x7fc00000u : __float_as_uint(res_score[rb][j][tid]);
+      uint16_t* dst = a.amax + (int64_t)d * n_entries + (int64_t)qwg * a.lq;
+      for (int e = tid; e < n_wg_e; e += kThreads) dst[e] = res_amax[rb][j][e];
     }
   };
 
   StageDesc cur, nxt, prv, prv2;
-  fetch_stage(cur);
+  fetch_stage(cur, 0);
   // The query operands and the first stage land together.  The operands must be resident
   // before the pipelined loop: otherwise their pending loads make the compiler wait for every
   // load in flight (the prefetch included) at each tile.
   __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
-  store_stage(0);
+  if constexpr (!DIRECT) store_stage(0);
   __syncthreads();
   bf16x8 fr[2][kRs];  // see step; region 0 of a stage's first tile is read after its barrier
 #pragma unroll
@@ -395,7 +456,11 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
     const int buf = stage & 1;
     const int rb = stage % 3;
     const bool more = prod.d < d_end;
-    if (more) fetch_stage(nxt);
+    if (more) fetch_stage(nxt, buf ^ 1);  // direct staging: into the other buffer, now idle
+    // direct staging: the results of two stages ago go out while the tiles run, so that the
+    // stage's closing wait for its loads finds the stores complete
+    if constexpr (DIRECT)
+      if (stage >= 2) write_results(prv2, (stage - 2) % 3);
     if (wave_active) {
 #pragma unroll
       for (int j = 0; j < kTps; ++j) {
@@ -417,8 +482,12 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
         ct = last ? 0 : ct + 1;
       }
     }
-    if (stage >= 2) write_results(prv2, (stage - 2) % 3);
-    if (more) store_stage(buf ^ 1);
+    if constexpr (DIRECT) {
+      __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this wave's loads of the next stage landed
+    } else {
+      if (stage >= 2) write_results(prv2, (stage - 2) % 3);
+      if (more) store_stage(buf ^ 1);
+    }
     __syncthreads();
     if (!more) break;
 #pragma unroll
@@ -446,10 +515,10 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
   write_results(cur, stage % 3);
 }
 
-template <int KS, int NB, int WPW>
+template <int KS, int NB, int WPW, bool DIRECT = false>
 hipError_t launch_argmax_t(const MaxsimPlan& plan, const MaxsimArgs& args, hipStream_t stream) {
   const int64_t blocks = (int64_t)plan.n_qgroups * plan.n_ranges;
-  hipLaunchKernelGGL((maxsim_argmax_kernel<KS, NB, WPW>), dim3((unsigned)blocks),
+  hipLaunchKernelGGL((maxsim_argmax_kernel<KS, NB, WPW, DIRECT>), dim3((unsigned)blocks),
                      dim3(64 * WPW), 0, stream, args, args.off);
   return hipGetLastError();
 }
@@ -461,7 +530,9 @@ hipError_t launch_argmax_variant(const MaxsimPlan& plan, const MaxsimArgs& args,
   switch (plan.ks) {
     case 2: return launch_argmax_t<2, 2, 4>(plan, args, stream);
     case 4: return launch_argmax_t<4, 2, 4>(plan, args, stream);
-    case 8: return launch_argmax_t<8, 2, 4>(plan, args, stream);
+    case 8:
+      return args.dim == 128 ? launch_argmax_t<8, 2, 4, true>(plan, args, stream)
+                             : launch_argmax_t<8, 2, 4>(plan, args, stream);
     case 16: return launch_argmax_t<16, 1, 4>(plan, args, stream);
     default: return hipErrorInvalidValue;
   }

@@ -345,6 +345,18 @@ def test_loss_over_thousands_of_short_documents():
     _loss_parity(Q, D, off, pos, 2.0)
 
 
+def test_loss_dim128_documents_ending_at_every_row_of_a_tile():
+    # at dim 128 the argmax kernel stages four tiles per stage straight into LDS: documents of
+    # 1-160 tokens end at every row of a tile and at every tile of a stage, and a stage holds
+    # tiles of several documents
+    nq, lq = 12, 32
+    g = torch.Generator().manual_seed(43)
+    lens = list(range(1, 161)) + torch.randint(1, 200, (60,), generator=g).tolist()
+    Q, D, off = _ragged(43, nq, lq, lens, 128)
+    pos = torch.randint(0, len(lens), (nq,), generator=g, dtype=torch.int32)
+    _loss_parity(Q, D, off, pos, 5.0)
+
+
 @pytest.mark.parametrize("nq,lq", [(200, 32), (470, 32)])
 def test_loss_many_query_tokens(nq, lq):
     # 6,400 and 15,040 (query, token) entries: the dD kernel's LDS no longer fits two 512-thread
