@@ -432,13 +432,14 @@ def test_loss_ranges_inside_a_long_document_and_over_many_tiny_ones():
         _loss_parity(Q, D, off, pos, 2.0)
 
 
-def test_loss_document_length_limit():
+@pytest.mark.parametrize("dim", [8, 128])  # tiles staged through VGPRs / straight into LDS
+def test_loss_document_length_limit(dim):
     # 65,536 tokens is the longest document whose argmax offsets fit 16 bits: such a document
     # is scored exactly; one token more and its scores, and hence the loss, are NaN.
-    Q, D, off = _ragged(3, 2, 4, [10, 65_536, 10], 8)
+    Q, D, off = _ragged(3, 2, 4, [10, 65_536, 10], dim)
     pos = torch.tensor([0, 2], dtype=torch.int32)
     _loss_parity(Q, D, off, pos, 1.0)
-    Q, D, off = _ragged(4, 2, 4, [10, 65_537, 10], 8)
+    Q, D, off = _ragged(4, 2, 4, [10, 65_537, 10], dim)
     r = hpr.coltrast_loss_fwd_bwd(*_to_dev(Q, D, off, pos), 1.0, return_scores=True)
     s = r["scores"].cpu().numpy()
     assert np.all(np.isnan(s[:, 1])) and math.isnan(float(r["loss"].item()))
