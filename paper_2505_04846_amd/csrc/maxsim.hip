@@ -39,12 +39,20 @@ namespace {
 // of k-step s of a lane sits at a fixed offset 32 s from a per-lane base (immediate offsets, no
 // per-read address arithmetic) and the 16 rows of a read phase start 16 bytes apart modulo the
 // 256-byte bank width (conflict-free); a stage holds kTps tiles.
-template <int KS>
+//
+// DIRECT (dim 128 with 128 query slots per wave, the many-query grids): the tiles go straight
+// from global memory into LDS (buffer loads with the LDS as destination), one tile per wave and
+// stage, so a stage holds WPW tiles.  A wave load writes 1 KiB of consecutive LDS bytes, so a
+// tile's region is rounded up to whole loads; the lanes that land on a row's padding or past
+// the tile's 32 rows load row 0 of the tile into bytes nobody reads.
+template <int KS, bool DIRECT = false, int WPW = 4>
 struct TileGeom {
   static constexpr int kCpr = KS * 2;              // 16-byte chunks per row
   static constexpr int kRowB = KS * 32 + 16;       // bytes per (padded) row
   static constexpr int kTileB = 32 * kRowB;        // bytes per tile
-  static constexpr int kTps = KS >= 8 ? 2 : 4;     // tiles per stage
+  static constexpr int kLoads = (kTileB + 1023) / 1024;             // direct loads per tile
+  static constexpr int kTileS = DIRECT ? kLoads * 1024 : kTileB;    // tile stride in a stage
+  static constexpr int kTps = DIRECT ? WPW : KS >= 8 ? 2 : 4;       // tiles per stage
 };
 
 
@@ -75,14 +83,20 @@ constexpr int maxsim_resident(int ks, int nb) {
 // MFMA before it (sched_group_barrier), so no second accumulator set is needed.  When the
 // previous tile ended its document, the document's scores are reduced (maximum over the
 // half-waves, sum over each query's slots) after the new tile's MFMAs are issued.
-template <int KS, int NB, int WPW>
+template <int KS, int NB, int WPW, bool DIRECT = false>
 __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB) * 4 / WPW)) void maxsim_kernel(
     MaxsimArgs a, const int64_t* __restrict__ off, const int64_t* __restrict__ part) {
-  using G = TileGeom<KS>;
+  using G = TileGeom<KS, DIRECT, WPW>;
   constexpr int kThreads = 64 * WPW;
   constexpr int kSlotsWG = WPW * NB * 32;
   constexpr int kTps = G::kTps;
-  __shared__ __attribute__((aligned(16))) unsigned char lds[2][kTps * G::kTileB];
+  static_assert(!DIRECT || NB == 4, "direct staging: the many-query variant (ordinary loads)");
+  // as many resident workgroups as the plan assumes (maxsim_resident): two stages and the ring
+  static_assert((maxsim_waves(KS, NB) * 4 / WPW) *
+                        (2 * kTps * G::kTileS + 3 * kTps * (kSlotsWG / 32) * 4) <=
+                    160 * 1024,
+                "LDS of the resident workgroups");
+  __shared__ __attribute__((aligned(16))) unsigned char lds[2][kTps * G::kTileS];
   // Per-document results, written to HBM after the barrier that follows the epilogue (a tile's
   // epilogue runs in the next tile's step, possibly in the next stage): a ring of three
   // stages, one slot per (tile, query of the workgroup).
@@ -178,7 +192,7 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB) * 4 / WPW)) void ma
   constexpr int kUpt = kTps * kPpt / kTpp;             // units per thread per stage
   TileCursor prod;
   open_doc(prod, d_begin);
-  u32x4 stage_regs[kUpt];
+  u32x4 stage_regs[DIRECT ? 1 : kUpt];
   const int lr = (tid / G::kCpr) & 31;            // row within the pass (within the tile)
   const int lt = __builtin_amdgcn_readfirstlane((tid / G::kCpr) >> 5);  // tile within the pass
   const int lc = tid % G::kCpr;
@@ -190,17 +204,48 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB) * 4 / WPW)) void ma
     __syncthreads();
   }
   const uint32_t row_bytes = 2u * (uint32_t)a.dim;
-  auto fetch_stage = [&](StageDesc& sd) {
+  // direct staging: this lane's source offset within the tile for load q of the tile (rows
+  // below 32 clamped to the tile's last row rmx; 0 for the lanes that fill padding)
+  auto direct_off = [&](int q, uint32_t rmx) {
+    const int p = q * 1024 + 16 * lane;
+    const int row = p / G::kRowB;
+    const int c = (p - row * G::kRowB) >> 4;
+    const uint32_t r = (uint32_t)row < rmx ? (uint32_t)row : rmx;
+    return (row < 32 && c < G::kCpr) ? r * (uint32_t)(32 * KS) + 16u * (uint32_t)c : 0u;
+  };
+  // direct staging: wave w loads tile w of the stage, whose first token is r0 and last row rmx
+  // (the lane offsets are recomputed per stage: kept, they would cost registers this kernel
+  // does not have)
+  auto issue_tile = [&](int buf, int r0, uint32_t rmx) {
+    const char* tptr = reinterpret_cast<const char*>(a.d) + (uint64_t)(uint32_t)r0 * row_bytes;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char*>(tptr), (short)0, 0x7fffffff, 0x00020000);
+    unsigned char* dst = &lds[buf][wave * G::kTileS];
+#pragma unroll
+    for (int q = 0; q < G::kLoads; ++q)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)(dst + 1024 * q), 16,
+                                               (int)direct_off(q, rmx), 0, 0, 0);
+  };
+  auto fetch_stage = [&](StageDesc& sd, int buf) {
     sd.d0 = prod.d;
     sd.t0 = prod.t;
     sd.valid = sd.last = sd.lng = 0u;
+    bool my_ok = false;
+    int my_r0 = 0;
+    uint32_t my_rmx = 0u;
 #pragma unroll
     for (int j = 0; j < kTps; ++j) {
       const bool ok = prod.d < d_end;
       const int r0 = ok ? prod.base + prod.t * 32 : 0;
       const uint32_t rmx = ok ? prod.len - prod.t * 32 - 1 : 0;  // later rows repeat the last
       const char* tptr = reinterpret_cast<const char*>(a.d) + (uint64_t)(uint32_t)r0 * row_bytes;
-      if (j % kTpp == lt && lok) {  // this thread's units of tile j
+      if constexpr (DIRECT) {
+        if (j == wave) {  // uniform
+          my_ok = ok;
+          my_r0 = r0;
+          my_rmx = rmx;
+        }
+      } else if (j % kTpp == lt && lok) {  // this thread's units of tile j
 #pragma unroll
         for (int p = 0; p < kPpt; ++p) {
           const uint32_t row = lr + kRp * p;
@@ -223,6 +268,8 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB) * 4 / WPW)) void ma
         }
       }
     }
+    if constexpr (DIRECT)
+      if (my_ok) issue_tile(buf, my_r0, my_rmx);
   };
   auto store_stage = [&](int buf) {
     if (!lok) return;
@@ -230,7 +277,7 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB) * 4 / WPW)) void ma
     for (int m = 0; m < kUpt; ++m) {
       const int j = (m / kPpt) * kTpp + lt;
       const uint32_t row = lr + kRp * (m % kPpt);
-      *reinterpret_cast<u32x4*>(&lds[buf][j * G::kTileB + row * G::kRowB + lboff]) =
+      *reinterpret_cast<u32x4*>(&lds[buf][j * G::kTileS + row * G::kRowB + lboff]) =
           stage_regs[m];
     }
   };
@@ -243,7 +290,7 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB) * 4 / WPW)) void ma
   const uint32_t a_lane = (uint32_t)(col * G::kRowB + half * 16);  // A: row col, chunk half
   auto frag = [&](int buf, int j, int s) {
     return as_bf16x8(
-        *reinterpret_cast<const u32x4*>(&lds[buf][j * G::kTileB] + a_lane + 32 * s));
+        *reinterpret_cast<const u32x4*>(&lds[buf][j * G::kTileS] + a_lane + 32 * s));
   };
 
   f32x16 acc[NB];
@@ -299,25 +346,24 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB) * 4 / WPW)) void ma
   };
 
   // Results of the documents that ended in a stage (ring slot rb) -> HBM (coalesced per doc).
+  // (the documents that end in a stage are consecutive from its first one, one per bit of
+  // `last`)
   auto write_results = [&](const StageDesc& sd, int rb) {
     int d = sd.d0;
 #pragma unroll 1
-    for (int j = 0; j < kTps; ++j) {
-      if (!((sd.valid >> j) & 1u)) break;
-      if ((sd.last >> j) & 1u) {
-        if (tid < n_wg_q) a.scores[(int64_t)(qwg + tid) * a.n_docs + d] = res_score[rb][j][tid];
-        ++d;
-      }
+    for (uint32_t m = sd.last & sd.valid; m != 0u; m &= m - 1u, ++d) {
+      const int j = __builtin_ctz(m);
+      if (tid < n_wg_q) a.scores[(int64_t)(qwg + tid) * a.n_docs + d] = res_score[rb][j][tid];
     }
   };
 
   StageDesc cur, nxt, prv, prv2;
-  fetch_stage(cur);
+  fetch_stage(cur, 0);
   // The query operands and the first stage land together.  The operands must be resident
   // before the pipelined loop: otherwise their pending loads make the compiler wait for every
   // load in flight (the prefetch included) at each tile.
   __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
-  store_stage(0);
+  if constexpr (!DIRECT) store_stage(0);
   __syncthreads();
   bf16x8 fr[2];
   fr[0] = frag(0, 0, 0);
@@ -351,7 +397,13 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB) * 4 / WPW)) void ma
     const int buf = stage & 1;
     const int rb = stage % 3;
     const bool more = prod.d < d_end;
-    if (more) fetch_stage(nxt);  // global loads in flight while this stage is computed
+    // global loads in flight while this stage is computed (direct staging: into the other
+    // buffer, idle since the last barrier)
+    if (more) fetch_stage(nxt, buf ^ 1);
+    // direct staging: the results of two stages ago go out while the tiles run, so that the
+    // stage's closing wait for its loads finds the stores complete
+    if constexpr (DIRECT)
+      if (stage >= 2) write_results(prv2, (stage - 2) % 3);
     if (wave_active) {
 #pragma unroll
       for (int j = 0; j < kTps; ++j) {
@@ -363,8 +415,12 @@ __global__ __launch_bounds__(64 * WPW, (maxsim_waves(KS, NB) * 4 / WPW)) void ma
         pend_j = j;
       }
     }
-    if (stage >= 2) write_results(prv2, (stage - 2) % 3);
-    if (more) store_stage(buf ^ 1);
+    if constexpr (DIRECT) {
+      __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this wave's loads of the next stage landed
+    } else {
+      if (stage >= 2) write_results(prv2, (stage - 2) % 3);
+      if (more) store_stage(buf ^ 1);
+    }
     __syncthreads();
     if (!more) break;
     if (sync && (stage & (kSyncStages - 1)) == kSyncStages - 1) {
@@ -441,10 +497,10 @@ __global__ void csr_validate_kernel(const int64_t* off, int64_t n_docs, int64_t 
 
 __global__ void fill_u64_kernel(unsigned long long* p, unsigned long long v) { *p = v; }
 
-template <int KS, int NB, int WPW>
+template <int KS, int NB, int WPW, bool DIRECT = false>
 hipError_t launch_t(const MaxsimPlan& plan, const MaxsimArgs& args, hipStream_t stream) {
-  hipLaunchKernelGGL((maxsim_kernel<KS, NB, WPW>), dim3((unsigned)plan.grid), dim3(64 * WPW), 0,
-                     stream, args, args.off, args.part);
+  hipLaunchKernelGGL((maxsim_kernel<KS, NB, WPW, DIRECT>), dim3((unsigned)plan.grid),
+                     dim3(64 * WPW), 0, stream, args, args.off, args.part);
   return hipGetLastError();
 }
 // Variants by k-steps of 16 (dim <= 16 KS) and query blocks per wave.  Query slots per wave:
@@ -463,6 +519,9 @@ hipError_t launch_variant(const MaxsimPlan& plan, const MaxsimArgs& args, bool a
     case 8 * 8 + 1: return launch_t<8, 1, 4>(plan, args, stream);
     case 8 * 8 + 2: return launch_t<8, 2, 4>(plan, args, stream);
     case 8 * 8 + 4:
+      if (args.dim == 128)
+        return plan.wpw == 8 ? launch_t<8, 4, 8, true>(plan, args, stream)
+                             : launch_t<8, 4, 4, true>(plan, args, stream);
       return plan.wpw == 8 ? launch_t<8, 4, 8>(plan, args, stream)
                            : launch_t<8, 4, 4>(plan, args, stream);
     case 16 * 8 + 1: return launch_t<16, 1, 4>(plan, args, stream);

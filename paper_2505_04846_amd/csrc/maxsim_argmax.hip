@@ -94,20 +94,6 @@ __device__ int range_first_doc(const int64_t* __restrict__ off, int64_t n_docs, 
   return (int)lo;
 }
 
-// half32_sum with its last step (the two 16-lane rows of each half-wave) through
-// v_permlane16_swap instead of an LDS permute: with both operands v, element 0 holds the even
-// row of each pair in both rows and element 1 the odd row, so their sum is the pair's total in
-// every lane (the same bits as v plus its partner row, addition being commutative).
-__device__ __forceinline__ float half32_sum_swap(float v) {
-  v += dpp_f<kDppQuadXor1>(v);
-  v += dpp_f<kDppQuadXor2>(v);
-  v += dpp_f<kDppRowHalfMirror>(v);
-  v += dpp_f<kDppRowMirror>(v);
-  const auto sw = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
-                                                   false);
-  return __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
-}
-
 template <int KS, int NB, int WPW, bool DIRECT>
 __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
     MaxsimArgs a, const int64_t* __restrict__ off) {
@@ -393,7 +379,7 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
         x = tk ? ox : x;
         if (half == 0 && slot_row[b] >= 0) res_amax[p.rb][p.j][slot_row[b]] = (uint16_t)x;
         bk[b] = INT32_MIN;
-        const float v = half32_sum_swap(slot_row[b] >= 0 ? m : 0.f);
+        const float v = half32_sum(slot_row[b] >= 0 ? m : 0.f);
         if ((my_blocks >> b) & 1u) qs += v;
       }
       if (lane < a.qpw) res_score[p.rb][p.j][wave * a.qpw + lane] = qs;

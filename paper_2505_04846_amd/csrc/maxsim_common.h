@@ -70,14 +70,18 @@ constexpr int kDppRowHalfMirror = 0x141;
 constexpr int kDppRowMirror = 0x140;
 
 // Sum over the 32 lanes l, l ^ 1, ..., of each half-wave in a fixed order; every lane of the
-// half gets the total.
+// half gets the total.  The last step adds the two 16-lane rows of each half through
+// v_permlane16_swap (no LDS round trip): with both operands v, element 0 holds the even row of
+// each pair in both rows and element 1 the odd row, so their sum is the pair's total in every
+// lane, the same bits whichever row a lane is in (addition being commutative).
 __device__ __forceinline__ float half32_sum(float v) {
   v += dpp_f<kDppQuadXor1>(v);
   v += dpp_f<kDppQuadXor2>(v);
   v += dpp_f<kDppRowHalfMirror>(v);  // quad q with quad 1 - q of the same half row
   v += dpp_f<kDppRowMirror>(v);      // the two half rows: the 16-lane row total
-  v += __shfl_xor(v, 16);            // the two rows of the half-wave
-  return v;
+  const auto sw = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                   false);
+  return __uint_as_float(sw[0]) + __uint_as_float(sw[1]);  // the two rows of the half-wave
 }
 
 // Workgroups of maxsim_argmax_kernel per CU: two by registers (its launch bounds), fewer when
