@@ -94,6 +94,16 @@ __device__ int range_first_doc(const int64_t* __restrict__ off, int64_t n_docs, 
   return (int)lo;
 }
 
+// A copy of a per-lane value that the compiler cannot see through: the ring addresses of the
+// per-document results are formed from it where they are used (once per document) instead of
+// being kept per (ring slot, tile) in registers that every stage would rotate.  Indexing the
+// ring as one flat array keeps the slot arithmetic scalar.
+__device__ __forceinline__ int opaque(int v) {
+  int r;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(r) : "v"(v));
+  return r;
+}
+
 template <int KS, int NB, int WPW, bool DIRECT>
 __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
     MaxsimArgs a, const int64_t* __restrict__ off) {
@@ -377,12 +387,14 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
                                                              false)[1];
         const bool tk = (otv > tv) | ((otv == tv) & (ox < x));
         x = tk ? ox : x;
-        if (half == 0 && slot_row[b] >= 0) res_amax[p.rb][p.j][slot_row[b]] = (uint16_t)x;
+        if (half == 0 && slot_row[b] >= 0)
+          res_amax[0][0][opaque(slot_row[b]) + (p.rb * kTps + p.j) * kSlotsWG] = (uint16_t)x;
         bk[b] = INT32_MIN;
         const float v = half32_sum(slot_row[b] >= 0 ? m : 0.f);
         if ((my_blocks >> b) & 1u) qs += v;
       }
-      if (lane < a.qpw) res_score[p.rb][p.j][wave * a.qpw + lane] = qs;
+      if (lane < a.qpw)
+        res_score[0][0][opaque(wave * a.qpw + lane) + (p.rb * kTps + p.j) * (kSlotsWG / 32)] = qs;
     }
   };
   // One pipelined step: the MFMAs of tile j (stage buffer `buf`) into X and, when HAS_Y, the
@@ -432,11 +444,14 @@ __global__ __launch_bounds__(64 * WPW, 2) void maxsim_argmax_kernel(
       // a document too long for 16-bit argmax offsets scores NaN, which the loss carries on
       // (stored as the bit pattern: this file is compiled assuming no NaN arithmetic)
       const bool lng = (sd.lng >> j) & 1u;
+      const int slot = rb * kTps + j;
       if (tid < n_wg_q)
         reinterpret_cast<uint32_t*>(a.scores)[(int64_t)(qwg + tid) * a.n_docs + d] =
-            lng ? 0x7fc00000u : __float_as_uint(res_score[rb][j][tid]);
+            lng ? 0x7fc00000u
+                : __float_as_uint(res_score[0][0][opaque(tid) + slot * (kSlotsWG / 32)]);
       uint16_t* dst = a.amax + (int64_t)d * n_entries + (int64_t)qwg * a.lq;
-      for (int e = tid; e < n_wg_e; e += kThreads) dst[e] = res_amax[rb][j][e];
+      for (int e = tid; e < n_wg_e; e += kThreads)
+        dst[e] = res_amax[0][0][opaque(e) + slot * kSlotsWG];
     }
   };
 
