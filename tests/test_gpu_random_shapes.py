@@ -86,6 +86,27 @@ def test_maxsim_score_random_shapes():
         _tight_scores(S, O, A, Qo, Do, off.numpy(), f"config {c} (tight)")
 
 
+def test_maxsim_score_dim128_many_query_slots():
+    # dim 128 with more than 256 query slots: the score kernel's variant that stages its tiles
+    # straight into LDS, four per stage (ragged documents end at every row of a tile and at any
+    # tile of a stage)
+    rng = np.random.default_rng(707)
+    for c in range(8):
+        lq = int(rng.integers(1, 129))
+        lqp = (lq + 31) // 32 * 32
+        nq = int(rng.integers(256 // lqp + 1, 257 // lqp + 40))
+        n_docs = int(rng.integers(1, 301))
+        max_len = int(rng.integers(1, 200))
+        print(f"config {c}: nq={nq} lq={lq} dim=128 n_docs={n_docs} max_len={max_len}",
+              flush=True)
+        Q, D, off = _store(rng, nq, lq, 128, n_docs, max_len, plant=c % 2 == 0)
+        S = hpr.maxsim_score(Q.to(DEV), D.to(DEV), off.to(DEV)).cpu().numpy()
+        Qo, Do = oracle.decode_bf16(_bits(Q)), oracle.decode_bf16(_bits(D))
+        O, A = oracle.maxsim_argmax(Qo, Do, off.numpy())
+        _close(S, O, REL, f"config {c}")
+        _tight_scores(S, O, A, Qo, Do, off.numpy(), f"config {c} (tight)")
+
+
 def test_maxsim_topk_random_shapes():
     rng = np.random.default_rng(202)
     for c in range(10):
