@@ -447,6 +447,22 @@ def test_loss_document_length_limit(dim):
     _assert_close(s[:, [0, 2]], o[:, [0, 2]], rel=1e-4, what="scores")
 
 
+@pytest.mark.parametrize("nq,lq,dim", [(12, 32, 128), (3, 20, 128), (9, 64, 128), (6, 17, 64),
+                                       (5, 32, 32), (4, 30, 256)])
+def test_loss_scores_equal_maxsim_score_bits(nq, lq, dim):
+    # The loss's argmax kernel and the score kernel take each tile's maximum in a different
+    # order but of the same fp32 products, and sum the query slots in the same fixed order: the
+    # scores the loss returns are maxsim_score's, bit for bit (different staging variants
+    # included: at dim 128 the first case takes the score kernel's directly staged one)
+    g = torch.Generator().manual_seed(nq * 1000 + lq + dim)
+    lens = torch.randint(1, 300, (57,), generator=g).tolist()
+    Q, D, off = _ragged(nq + dim, nq, lq, lens, dim)
+    pos = torch.randint(0, len(lens), (nq,), generator=g, dtype=torch.int32)
+    Qd, Dd, od, pd = _to_dev(Q, D, off, pos)
+    r = hpr.coltrast_loss_fwd_bwd(Qd, Dd, od, pd, 2.0, return_scores=True)
+    assert torch.equal(r["scores"], hpr.maxsim_score(Qd, Dd, od))
+
+
 def test_loss_grads_optional_and_deterministic():
     w = synth.coltrast_step(seed=1, nq=8, n_neg=3, ld=64)
     args = _to_dev(w["Q"], w["D"], w["off"], w["pos"])
