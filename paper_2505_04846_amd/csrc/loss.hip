@@ -117,7 +117,10 @@ __global__ __launch_bounds__(kRowThreads) void infonce_kernel(const float* __res
   const bool bad = p < 0 || p >= n;
   float term = 0.f;
   if (bad) {
-    for (int64_t d = tid; d < n; d += kRowThreads) Gq[d] = 0.f;
+    each([&](int64_t d, float sd) {
+      if (scores_out) scores_out[(int64_t)q * n + d] = sd;
+      Gq[d] = 0.f;
+    });
     if (tid == 0) atomicOr(&ctrl[0], 2);
   } else {
     term = (M - (s * Sq[p])) + l1p;

@@ -481,8 +481,13 @@ def test_loss_bad_positive_gives_nan():
     w = synth.coltrast_step(seed=2, nq=4, n_neg=1, ld=32)
     pos = w["pos"].clone()
     pos[1] = 10_000
-    r = hpr.coltrast_loss_fwd_bwd(*_to_dev(w["Q"], w["D"], w["off"], pos), 1.0)
+    args = _to_dev(w["Q"], w["D"], w["off"], pos)
+    r = hpr.coltrast_loss_fwd_bwd(*args, 1.0, return_scores=True)
     assert math.isnan(float(r["loss"].item()))
+    # the scores are still returned whole, the bad row's included
+    assert torch.equal(r["scores"], hpr.maxsim_score(*args[:3]))
+    # the bad row's G is zero: its query tokens get no MaxSim gradient
+    assert not bool(r["dq"][1].any())
 
 
 def test_autograd_function_matches_fwd_bwd_and_scales():
